@@ -1,0 +1,130 @@
+"""fp64 CPU oracle for SD attention -- TEST INFRASTRUCTURE ONLY.
+
+Only the tests, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package.  The product library never does, and
+this package imports nothing from the product.
+
+It binds ``liboracle.so`` (built from ``oracle.c``; see that file for the
+passages of the paper each function follows):
+
+* :func:`attention` -- Eq. 3 in three passes per row (max, exp-sum,
+  normalise times V), returning O and Eq. 4's L and S.
+* :func:`softmax_rows` -- Eq. 4's reduction (L, S) on a given matrix and the
+  element-wise step p = exp(a - L) / S.
+
+Inputs are numpy arrays: float16, float32, float64, or bfloat16 passed as a
+uint16 bit-pattern array with ``dtype="bf16"``.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+from . import build as _build
+
+_F16, _BF16, _F32, _F64 = 0, 1, 2, 3
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_build.LIB) or (
+                os.path.getmtime(_build.LIB) < os.path.getmtime(_build.SRC)):
+            _build.build()
+        lib = ctypes.CDLL(_build.LIB)
+        vp, i32, i64, f32 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_float
+        lib.oracle_attention_f64.argtypes = [vp, vp, vp, i32, i32, i32, i32, i32, i32,
+                                             f32, vp, i64, i32, vp, vp, vp]
+        lib.oracle_attention_f64.restype = i32
+        lib.oracle_softmax_rows_f64.argtypes = [vp, i32, i64, i64, f32, i32, vp, vp]
+        lib.oracle_softmax_rows_f64.restype = i32
+        lib.oracle_widen.argtypes = [vp, i32, i64, vp]
+        lib.oracle_widen.restype = i32
+        lib.oracle_num_threads.argtypes = [i32]
+        lib.oracle_num_threads.restype = i32
+        _lib = lib
+    return _lib
+
+
+def _code(arr, dtype):
+    if dtype == "bf16":
+        if arr.dtype != np.uint16:
+            raise TypeError("bf16 inputs are passed as uint16 bit patterns")
+        return _BF16
+    if dtype is not None and dtype != "auto":
+        raise ValueError(f"unknown dtype tag {dtype!r}")
+    return {np.dtype(np.float16): _F16, np.dtype(np.float32): _F32,
+            np.dtype(np.float64): _F64}[arr.dtype]
+
+
+def _ptr(a):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def num_threads(requested: int = 0) -> int:
+    """Threads the oracle's OpenMP regions use for ``requested`` (0 = default)."""
+    return _load().oracle_num_threads(int(requested))
+
+
+def widen(x, dtype=None):
+    """Exact widening of a float16 / bfloat16 (uint16) / float32 array to float64."""
+    x = np.ascontiguousarray(x)
+    code = _code(x, dtype)
+    out = np.empty(x.shape, dtype=np.float64)
+    if _load().oracle_widen(_ptr(x), code, x.size, _ptr(out)) != 0:
+        raise ValueError("oracle_widen rejected its arguments")
+    return out
+
+
+def attention(q, k, v, scale, rows=None, dtype=None, nthreads=0):
+    """Eq. 3 in fp64.  q: [B,H,Lq,D], k, v: [B,H,Lk,D], same element type.
+
+    rows: optional 1-D array of flat query-row indices (b*H + h)*Lq + i; the
+    outputs then hold only those rows, in that order.
+    Returns (O, L, S): O is [B,H,Lq,D] (or [len(rows), D]); L and S are
+    Eq. 4's row maximum and shifted exponential sum, shaped like O[..., 0].
+    """
+    q, k, v = (np.ascontiguousarray(t) for t in (q, k, v))
+    if q.ndim != 4 or k.shape != v.shape or q.shape[:2] != k.shape[:2] or q.shape[3] != k.shape[3]:
+        raise ValueError("expected q [B,H,Lq,D] and k, v [B,H,Lk,D]")
+    if not (q.dtype == k.dtype == v.dtype):
+        raise TypeError("q, k and v must share one element type")
+    B, H, Lq, D = q.shape
+    Lk = k.shape[2]
+    code = _code(q, dtype)
+    if rows is None:
+        n, rp, shape = B * H * Lq, None, (B, H, Lq)
+    else:
+        rows = np.ascontiguousarray(rows, dtype=np.int64)
+        n, rp, shape = rows.size, _ptr(rows), (rows.size,)
+    out = np.empty(shape + (D,), dtype=np.float64)
+    L = np.empty(shape, dtype=np.float64)
+    S = np.empty(shape, dtype=np.float64)
+    rc = _load().oracle_attention_f64(_ptr(q), _ptr(k), _ptr(v), code, B, H, Lq, Lk, D,
+                                      float(np.float32(scale)), rp, n, int(nthreads),
+                                      _ptr(out), _ptr(L), _ptr(S))
+    if rc != 0:
+        raise ValueError("oracle_attention_f64 rejected its arguments")
+    return out, L, S
+
+
+def softmax_rows(a, scale=1.0, want_p=False, dtype=None, nthreads=0):
+    """Eq. 4 on a [rows, cols] matrix with a_ij = scale * A_ij.
+
+    Returns (L, S) and, if want_p, also p = exp(a - L) / S (all fp64).
+    """
+    a = np.ascontiguousarray(a)
+    if a.ndim != 2:
+        raise ValueError("expected a 2-D matrix")
+    code = _code(a, dtype)
+    rows, cols = a.shape
+    ls = np.empty((rows, 2), dtype=np.float64)
+    p = np.empty((rows, cols), dtype=np.float64) if want_p else None
+    rc = _load().oracle_softmax_rows_f64(_ptr(a), code, rows, cols, float(np.float32(scale)),
+                                         int(nthreads), _ptr(ls), _ptr(p) if want_p else None)
+    if rc != 0:
+        raise ValueError("oracle_softmax_rows_f64 rejected its arguments")
+    if want_p:
+        return ls[:, 0], ls[:, 1], p
+    return ls[:, 0], ls[:, 1]

@@ -1,0 +1,207 @@
+/*
+ * oracle.c -- plain, slow, fp64 CPU reference for the attention of
+ * "Speed Is All You Need: On-Device Acceleration of Large Diffusion Models via
+ * GPU-Aware Optimizations" (Chen et al., CVPR 2023 workshop).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may call, link or
+ * load this file; only the tests, the smoke check and the CPU-baseline leg
+ * of the benchmark do.  It shares no code, header, table or helper with the
+ * HIP library.
+ *
+ * What it computes (Sec. 3.2.1 "Partially Fused Softmax"):
+ *   Eq. 3  Attention(Q, K, V) = softmax(Q K^T / sqrt(d)) V,
+ *          Q in R^{N x d}, K, V in R^{M x d}.
+ *   Eq. 4  L_i = max_j a_ij,  S_i = sum_j exp(a_ij - max_k a_ik)  for the
+ *          matrix A = Q K^T / sqrt(d), followed by the element-wise
+ *          normalisation exp(a_ij - L_i) / S_i (the text after Eq. 4).
+ *
+ * Each output row is computed in three passes, exactly as the definition
+ * reads: (1) the logits a_ij and their maximum L_i, (2) the shifted
+ * exponential sum S_i, (3) the normalised weights times V.  All arithmetic is
+ * IEEE double with libm exp; inputs are widened exactly from binary16,
+ * bfloat16 or binary32; the scale is the binary32 value the GPU receives,
+ * widened exactly.  The caller picks the scale (1/sqrt(d) with the true head
+ * dimension d in the UNet).  No blocking, fusion or reordering beyond the
+ * definition.  Rows are independent, so OpenMP splits the work by row; the
+ * result does not depend on the thread count.
+ *
+ * Build: gcc -O2 -fopenmp -fPIC -shared (no -ffast-math).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* element type codes of the oracle's inputs */
+enum { OR_F16 = 0, OR_BF16 = 1, OR_F32 = 2, OR_F64 = 3 };
+
+/* IEEE 754 binary16 -> double, from the format's definition:
+ * 1 sign bit, 5 exponent bits (bias 15), 10 fraction bits. */
+static double or_from_binary16(uint16_t bits)
+{
+    const int sign = bits >> 15;
+    const int expo = (bits >> 10) & 0x1f;
+    const int frac = bits & 0x3ff;
+    double mag;
+    if (expo == 0)            /* zero or subnormal: frac * 2^-24 */
+        mag = ldexp((double)frac, -24);
+    else if (expo == 31)      /* infinity or NaN */
+        mag = frac ? NAN : INFINITY;
+    else                      /* normal: (1024 + frac) * 2^(expo - 25) */
+        mag = ldexp((double)(frac | 0x400), expo - 25);
+    return sign ? -mag : mag;
+}
+
+/* bfloat16 is the upper half of a binary32 word */
+static double or_from_bfloat16(uint16_t bits)
+{
+    uint32_t word = (uint32_t)bits << 16;
+    float f;
+    memcpy(&f, &word, sizeof f);
+    return (double)f;
+}
+
+static double or_elem(const void *base, int dtype, int64_t idx)
+{
+    switch (dtype) {
+    case OR_F16:  return or_from_binary16(((const uint16_t *)base)[idx]);
+    case OR_BF16: return or_from_bfloat16(((const uint16_t *)base)[idx]);
+    case OR_F32:  return (double)((const float *)base)[idx];
+    default:      return ((const double *)base)[idx];
+    }
+}
+
+int oracle_num_threads(int requested)
+{
+#ifdef _OPENMP
+    return requested > 0 ? requested : omp_get_max_threads();
+#else
+    (void)requested;
+    return 1;
+#endif
+}
+
+/* Widen n elements of `src` (type `dtype`) into `dst` as double. */
+int oracle_widen(const void *src, int dtype, int64_t n, double *dst)
+{
+    if (!src || !dst || n < 0 || dtype < OR_F16 || dtype > OR_F64)
+        return 1;
+    for (int64_t i = 0; i < n; ++i)
+        dst[i] = or_elem(src, dtype, i);
+    return 0;
+}
+
+/*
+ * Attention, Eq. 3, for Q [B,H,Lq,D], K and V [B,H,Lk,D] (contiguous,
+ * D innermost), all of element type `dtype`.
+ *
+ * rows: NULL for every query row, else `nrows` flat row indices
+ *       r = (b*H + h)*Lq + i selecting the rows to compute.
+ * out:  [nrows or B*H*Lq][D] doubles, row by row in the order asked for.
+ * L, S: optional [same rows] doubles receiving Eq. 4's L_i and S_i.
+ * Returns 0, or 1 on a bad argument.
+ */
+int oracle_attention_f64(const void *q, const void *k, const void *v, int dtype,
+                         int B, int H, int Lq, int Lk, int D, float scale,
+                         const int64_t *rows, int64_t nrows, int nthreads,
+                         double *out, double *L, double *S)
+{
+    if (!q || !k || !v || !out || B < 1 || H < 1 || Lq < 1 || Lk < 1 || D < 1 ||
+        dtype < OR_F16 || dtype > OR_F64)
+        return 1;
+    const int64_t total = (int64_t)B * H * Lq;
+    const int64_t n = rows ? nrows : total;
+    if (n < 0)
+        return 1;
+    if (rows)
+        for (int64_t t = 0; t < n; ++t)
+            if (rows[t] < 0 || rows[t] >= total)
+                return 1;
+    const double sc = (double)scale;
+    int bad = 0;
+
+#pragma omp parallel num_threads(oracle_num_threads(nthreads)) reduction(| : bad)
+    {
+        double *a = (double *)malloc(sizeof(double) * (size_t)Lk);
+        if (!a) {
+            bad = 1;
+        } else {
+#pragma omp for schedule(static)
+            for (int64_t t = 0; t < n; ++t) {
+                const int64_t r = rows ? rows[t] : t;
+                const int64_t bh = r / Lq;             /* (b, h) pair */
+                const int64_t qrow = r * D;            /* start of q_i */
+                const int64_t kv0 = bh * Lk * D;       /* start of K, V of this head */
+
+                /* pass 1: a_ij = scale * <q_i, k_j>, and L_i = max_j a_ij */
+                double Li = -INFINITY;
+                for (int j = 0; j < Lk; ++j) {
+                    double dot = 0.0;
+                    for (int d = 0; d < D; ++d)
+                        dot += or_elem(q, dtype, qrow + d) *
+                               or_elem(k, dtype, kv0 + (int64_t)j * D + d);
+                    a[j] = sc * dot;
+                    if (a[j] > Li)
+                        Li = a[j];
+                }
+                /* pass 2: S_i = sum_j exp(a_ij - L_i) */
+                double Si = 0.0;
+                for (int j = 0; j < Lk; ++j)
+                    Si += exp(a[j] - Li);
+                /* pass 3: o_i = sum_j exp(a_ij - L_i) / S_i * v_j */
+                double *o = out + t * D;
+                for (int d = 0; d < D; ++d)
+                    o[d] = 0.0;
+                for (int j = 0; j < Lk; ++j) {
+                    const double pij = exp(a[j] - Li) / Si;
+                    for (int d = 0; d < D; ++d)
+                        o[d] += pij * or_elem(v, dtype, kv0 + (int64_t)j * D + d);
+                }
+                if (L)
+                    L[t] = Li;
+                if (S)
+                    S[t] = Si;
+            }
+            free(a);
+        }
+    }
+    return bad;
+}
+
+/*
+ * The reduction step of Eq. 4 on a given matrix A [rows][cols] of type
+ * `dtype`, with the scale applied first (a_ij = scale * A_ij):
+ *   ls[2r]   = L_r = max_j a_rj
+ *   ls[2r+1] = S_r = sum_j exp(a_rj - L_r)
+ * and, when p is not NULL, the element-wise step p_rj = exp(a_rj - L_r) / S_r.
+ */
+int oracle_softmax_rows_f64(const void *a, int dtype, int64_t rows, int64_t cols,
+                            float scale, int nthreads, double *ls, double *p)
+{
+    if (!a || !ls || rows < 1 || cols < 1 || dtype < OR_F16 || dtype > OR_F64)
+        return 1;
+    const double sc = (double)scale;
+
+#pragma omp parallel for schedule(static) num_threads(oracle_num_threads(nthreads))
+    for (int64_t r = 0; r < rows; ++r) {
+        const int64_t base = r * cols;
+        double Lr = -INFINITY;
+        for (int64_t j = 0; j < cols; ++j) {
+            const double x = sc * or_elem(a, dtype, base + j);
+            if (x > Lr)
+                Lr = x;
+        }
+        double Sr = 0.0;
+        for (int64_t j = 0; j < cols; ++j)
+            Sr += exp(sc * or_elem(a, dtype, base + j) - Lr);
+        ls[2 * r] = Lr;
+        ls[2 * r + 1] = Sr;
+        if (p)
+            for (int64_t j = 0; j < cols; ++j)
+                p[base + j] = exp(sc * or_elem(a, dtype, base + j) - Lr) / Sr;
+    }
+    return 0;
+}

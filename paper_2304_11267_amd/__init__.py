@@ -1,0 +1,13 @@
+"""sdattn for MI355X: SD1.4 UNet attention as hand-written HIP kernels for gfx950.
+
+The compute lives in ``libsdattn.so`` (C ABI declared in ``include/sdattn.h``).
+This package is a thin binding: it marshals torch tensors' device pointers and
+the current HIP stream into that library and raises on a nonzero status.  The
+library is loaded on first use; if it is missing the call raises instead of
+falling back to anything else.
+"""
+from .binding import (  # noqa: F401
+    SdattnError, forward, forward_ex, softmax_rows, library_path, load_library,
+    STATUS_OK, STATUS_INVALID_ARG, STATUS_UNSUPPORTED, STATUS_MISALIGNED, STATUS_HIP,
+    DTYPE_F16, DTYPE_BF16, DTYPE_F32,
+)

@@ -1,0 +1,137 @@
+"""ctypes binding of libsdattn.so (argument marshalling only).
+
+Every function takes torch tensors that already live on the GPU, passes their
+device pointers, sizes and the current HIP stream to the C entry point of the
+same name, and raises :class:`SdattnError` on a nonzero status.  No
+arithmetic of the attention happens here.  The library is loaded from the
+package directory on first use; a missing library raises, there is no other
+code path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_NAME = "libsdattn.so"
+
+STATUS_OK = 0
+STATUS_INVALID_ARG = 1
+STATUS_UNSUPPORTED = 2
+STATUS_MISALIGNED = 3
+STATUS_HIP = 4
+
+DTYPE_F16 = 0
+DTYPE_BF16 = 1
+DTYPE_F32 = 2
+
+# every symbol include/sdattn.h declares
+EXPORTS = ("sdattn_forward", "sdattn_forward_ex", "sdattn_softmax_rows",
+           "sdattn_status_str", "sdattn_last_hip_error", "sdattn_version")
+
+_lib = None
+
+
+class SdattnError(RuntimeError):
+    def __init__(self, fn: str, status: int, hip_error: int, text: str):
+        super().__init__(f"{fn} failed: status {status} ({text}), hip error {hip_error}")
+        self.status = status
+        self.hip_error = hip_error
+
+
+def library_path() -> str:
+    return os.environ.get("SDATTN_LIBRARY", os.path.join(HERE, LIB_NAME))
+
+
+def load_library():
+    """Load libsdattn.so and declare its signatures (raises if it is missing)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    path = library_path()
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built; run __graft_entry__.build() "
+                           "(the HIP library is the only implementation)")
+    lib = ctypes.CDLL(path)
+    vp, i32, i64, f32 = ctypes.c_void_p, ctypes.c_int, ctypes.c_longlong, ctypes.c_float
+    lib.sdattn_forward.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, f32, vp]
+    lib.sdattn_forward.restype = i32
+    lib.sdattn_forward_ex.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, f32, i32, vp]
+    lib.sdattn_forward_ex.restype = i32
+    lib.sdattn_softmax_rows.argtypes = [vp, vp, vp, i64, i64, f32, i32, vp]
+    lib.sdattn_softmax_rows.restype = i32
+    lib.sdattn_status_str.argtypes = [i32]
+    lib.sdattn_status_str.restype = ctypes.c_char_p
+    lib.sdattn_last_hip_error.argtypes = []
+    lib.sdattn_last_hip_error.restype = i32
+    lib.sdattn_version.argtypes = []
+    lib.sdattn_version.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def _check(fn: str, status: int):
+    if status != STATUS_OK:
+        lib = load_library()
+        raise SdattnError(fn, status, lib.sdattn_last_hip_error(),
+                          lib.sdattn_status_str(status).decode())
+
+
+def _dtype_code(t):
+    import torch
+    if t.dtype == torch.float16:
+        return DTYPE_F16
+    if t.dtype == torch.bfloat16:
+        return DTYPE_BF16
+    if t.dtype == torch.float32:
+        return DTYPE_F32
+    raise TypeError(f"unsupported element type {t.dtype}")
+
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dev(t, name):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def forward(q, k, v, out, scale: float, stream=None):
+    """out = softmax(scale * q k^T) v for q/out [B,H,Lq,D], k/v [B,H,Lk,D], fp16."""
+    B, H, Lq, D = q.shape
+    Lk = k.shape[2]
+    status = load_library().sdattn_forward(
+        _dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(out, "out"),
+        B, H, Lq, Lk, D, ctypes.c_float(scale), _stream(stream))
+    _check("sdattn_forward", status)
+    return out
+
+
+def forward_ex(q, k, v, out, scale: float, ls=None, stream=None):
+    """forward for fp16 or bf16, optionally writing fp32 (L, S) per row to ls [B,H,Lq,2]."""
+    B, H, Lq, D = q.shape
+    Lk = k.shape[2]
+    ls_ptr = _dev(ls, "ls") if ls is not None else None
+    status = load_library().sdattn_forward_ex(
+        _dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(out, "out"), ls_ptr,
+        B, H, Lq, Lk, D, ctypes.c_float(scale), _dtype_code(q), _stream(stream))
+    _check("sdattn_forward_ex", status)
+    return out
+
+
+def softmax_rows(a, ls, p=None, scale: float = 1.0, stream=None):
+    """Eq. 4 on a [rows, cols]: ls[r] = (L_r, S_r) fp32; p (optional) = exp(scale*a - L)/S."""
+    rows, cols = a.shape
+    p_ptr = _dev(p, "p") if p is not None else None
+    status = load_library().sdattn_softmax_rows(
+        _dev(a, "a"), _dev(ls, "ls"), p_ptr, rows, cols, ctypes.c_float(scale),
+        _dtype_code(a), _stream(stream))
+    _check("sdattn_softmax_rows", status)
+    return ls

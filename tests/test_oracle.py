@@ -1,0 +1,357 @@
+"""Pins of the fp64 oracle against facts it must reproduce (CPU only).
+
+Each pin is something other than the oracle's own formula: exact decoding
+against numpy's float16 routine, a 50-digit brute force of Eq. 3 written
+without the max subtraction, closed forms (constant keys, zero scale, one key,
+constant value columns, identity values), invariants (joint key/value
+permutation, linearity in V, shift invariance of Eq. 4), the block-merge rule
+of the multi-stage reduction (Sec. 3.2.1), and torch's fp64 CPU attention and
+softmax as independent library routines.  A dropped term, a wrong sign, a
+wrong scale, a transposed operand or a wrong row index fails at least one.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2304_11267_amd import workloads as wl
+
+mpmath = pytest.importorskip("mpmath")
+
+
+def _rand16(rng, shape, mult=1.0):
+    return (rng.standard_normal(shape, dtype=np.float32) * np.float32(mult)).astype(np.float16)
+
+
+# ----------------------------------------------------------------- decoding
+
+def test_widen_binary16_every_bit_pattern():
+    bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    h = bits.view(np.float16)
+    got = oracle.widen(h)
+    ref = h.astype(np.float64)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], ref[~nan])
+    # signed zeros keep their sign
+    assert np.array_equal(np.signbit(got[~nan]), np.signbit(ref[~nan]))
+
+
+def test_widen_bfloat16_matches_float32_upper_half():
+    rng = np.random.default_rng(7)
+    bits = rng.integers(0, 65536, size=20000, dtype=np.uint32).astype(np.uint16)
+    got = oracle.widen(bits, dtype="bf16")
+    with np.errstate(invalid="ignore"):
+        ref = (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], ref[~nan])
+
+
+# ------------------------------------------------------ brute force, Eq. 3
+
+def _brute_force(q, k, v, scale):
+    """Eq. 3 at 50 digits, direct form sum_j e^{s_j} v_j / sum_j e^{s_j}."""
+    mp = mpmath.mp
+    mp.dps = 50
+    B, H, Lq, D = q.shape
+    Lk = k.shape[2]
+    qf, kf, vf = (t.astype(np.float64) for t in (q, k, v))
+    sc = mpmath.mpf(float(np.float32(scale)))
+    out = np.zeros((B, H, Lq, D))
+    Ls = np.zeros((B, H, Lq))
+    Ss = np.zeros((B, H, Lq))
+    for b in range(B):
+        for h in range(H):
+            for i in range(Lq):
+                s = [sc * mpmath.fsum(mpmath.mpf(float(qf[b, h, i, d])) * mpmath.mpf(float(kf[b, h, j, d]))
+                                      for d in range(D)) for j in range(Lk)]
+                w = [mpmath.exp(x) for x in s]
+                tot = mpmath.fsum(w)
+                for d in range(D):
+                    out[b, h, i, d] = float(mpmath.fsum(w[j] * mpmath.mpf(float(vf[b, h, j, d]))
+                                                        for j in range(Lk)) / tot)
+                L = max(s)
+                Ls[b, h, i] = float(L)
+                Ss[b, h, i] = float(mpmath.fsum(mpmath.exp(x - L) for x in s))
+    return out, Ls, Ss
+
+
+BRUTE_SHAPES = [
+    # (B, H, Lq, Lk, D, q_mult, scale or None for 1/sqrt(D))
+    (1, 1, 1, 1, 8, 1.0, None),
+    (1, 1, 3, 5, 8, 1.0, None),
+    (2, 2, 4, 7, 16, 1.0, None),
+    (1, 2, 8, 8, 40, 1.0, None),
+    (1, 1, 5, 3, 24, 1.0, None),
+    (1, 1, 6, 8, 16, 8.0, 1.0),     # logits in the hundreds: needs the max shift
+    (1, 1, 4, 6, 8, 4.0, -0.75),    # negative scale
+]
+
+
+@pytest.mark.parametrize("shape", BRUTE_SHAPES)
+def test_brute_force_small(shape):
+    B, H, Lq, Lk, D, mult, scale = shape
+    rng = np.random.default_rng(1000 + Lq * 31 + Lk * 7 + D)
+    q = _rand16(rng, (B, H, Lq, D), mult)
+    k = _rand16(rng, (B, H, Lk, D))
+    v = _rand16(rng, (B, H, Lk, D))
+    if scale is None:
+        scale = float(np.float32(1 / np.sqrt(D)))
+    o, L, S = oracle.attention(q, k, v, scale)
+    ro, rL, rS = _brute_force(q, k, v, scale)
+    vmax = np.abs(v.astype(np.float64)).max()
+    assert np.max(np.abs(o - ro)) <= 1e-12 * vmax
+    assert np.max(np.abs(L - rL) / np.maximum(1.0, np.abs(rL))) <= 1e-12
+    assert np.max(np.abs(S - rS) / rS) <= 1e-12
+
+
+# --------------------------------------------------------------- structure
+
+def test_row_subset_and_thread_count_do_not_change_results():
+    rng = np.random.default_rng(3)
+    q = _rand16(rng, (2, 3, 37, 24))
+    k = _rand16(rng, (2, 3, 29, 24))
+    v = _rand16(rng, (2, 3, 29, 24))
+    full, L, S = oracle.attention(q, k, v, 0.2, nthreads=1)
+    full8, L8, S8 = oracle.attention(q, k, v, 0.2, nthreads=8)
+    assert np.array_equal(full, full8) and np.array_equal(L, L8) and np.array_equal(S, S8)
+    rows = np.array([0, 5, 36, 37, 100, 221, 2 * 3 * 37 - 1])
+    sub, Ls, Ss = oracle.attention(q, k, v, 0.2, rows=rows)
+    flat = full.reshape(-1, 24)
+    assert np.array_equal(sub, flat[rows])
+    assert np.array_equal(Ls, L.reshape(-1)[rows])
+    assert np.array_equal(Ss, S.reshape(-1)[rows])
+
+
+def test_constant_keys_give_mean_of_values():
+    rng = np.random.default_rng(4)
+    q = _rand16(rng, (2, 2, 9, 40))
+    k = np.broadcast_to(_rand16(rng, (2, 2, 1, 40)), (2, 2, 13, 40)).copy()
+    v = _rand16(rng, (2, 2, 13, 40))
+    o, _, S = oracle.attention(q, k, v, 0.3)
+    ref = v.astype(np.float64).mean(axis=2, keepdims=True)
+    assert np.max(np.abs(o - ref)) <= 1e-14
+    assert np.allclose(S, 13.0, rtol=0, atol=1e-12)
+
+
+def test_zero_scale_gives_mean_of_values():
+    rng = np.random.default_rng(5)
+    q, k, v = (_rand16(rng, (1, 2, n, 16)) for n in (5, 11, 11))
+    o, L, S = oracle.attention(q, k, v, 0.0)
+    assert np.max(np.abs(o - v.astype(np.float64).mean(axis=2, keepdims=True))) <= 1e-14
+    assert np.all(L == 0.0) and np.all(S == 11.0)
+
+
+def test_single_key_returns_its_value_exactly():
+    rng = np.random.default_rng(6)
+    q = _rand16(rng, (2, 2, 7, 32), 3.0)
+    k = _rand16(rng, (2, 2, 1, 32))
+    v = _rand16(rng, (2, 2, 1, 32))
+    o, _, S = oracle.attention(q, k, v, 0.5)
+    assert np.array_equal(o, np.broadcast_to(v.astype(np.float64), o.shape))
+    assert np.all(S == 1.0)
+
+
+def test_constant_value_columns_give_the_constant():
+    rng = np.random.default_rng(8)
+    q = _rand16(rng, (1, 2, 6, 16), 2.0)
+    k = _rand16(rng, (1, 2, 19, 16))
+    cols = _rand16(rng, (1, 2, 1, 16))
+    v = np.broadcast_to(cols, (1, 2, 19, 16)).copy()
+    o, _, _ = oracle.attention(q, k, v, 0.25)
+    ref = np.broadcast_to(cols.astype(np.float64), o.shape)
+    assert np.max(np.abs(o - ref) / np.maximum(np.abs(ref), 1e-300)) <= 1e-14
+
+
+def test_identity_values_reproduce_softmax_rows():
+    """V = I with Lk = D gives O = P, the element-wise step of Eq. 4."""
+    rng = np.random.default_rng(9)
+    D = 16
+    q = _rand16(rng, (1, 1, 10, D), 2.0)
+    k = _rand16(rng, (1, 1, D, D))
+    v = np.eye(D, dtype=np.float16)[None, None]
+    scale = 0.35
+    o, L, S = oracle.attention(q, k, v, scale)
+    a = q[0, 0].astype(np.float64) @ k[0, 0].astype(np.float64).T   # library matmul
+    Lr, Sr, P = oracle.softmax_rows(a, scale=scale, want_p=True)
+    assert np.max(np.abs(o[0, 0] - P)) <= 1e-14
+    assert np.max(np.abs(L[0, 0] - Lr)) <= 1e-13
+    assert np.max(np.abs(S[0, 0] - Sr) / Sr) <= 1e-13
+
+
+def test_joint_key_value_permutation_invariance():
+    rng = np.random.default_rng(10)
+    q = _rand16(rng, (2, 2, 8, 40), 2.0)
+    k = _rand16(rng, (2, 2, 77, 40))
+    v = _rand16(rng, (2, 2, 77, 40))
+    perm = rng.permutation(77)
+    o1, L1, S1 = oracle.attention(q, k, v, 0.158)
+    o2, L2, S2 = oracle.attention(q, k[:, :, perm].copy(), v[:, :, perm].copy(), 0.158)
+    assert np.max(np.abs(o1 - o2)) <= 1e-13
+    assert np.array_equal(L1, L2)
+    assert np.max(np.abs(S1 - S2) / S1) <= 1e-13
+    # permuting keys alone does change the output (the pairing matters)
+    o3, _, _ = oracle.attention(q, k[:, :, perm].copy(), v, 0.158)
+    assert np.max(np.abs(o1 - o3)) > 1e-2
+
+
+def test_linear_in_values():
+    rng = np.random.default_rng(11)
+    q = rng.standard_normal((1, 2, 5, 8))
+    k = rng.standard_normal((1, 2, 9, 8))
+    v1 = rng.standard_normal((1, 2, 9, 8))
+    v2 = rng.standard_normal((1, 2, 9, 8))
+    o1, _, _ = oracle.attention(q, k, v1, 0.4)
+    o2, _, _ = oracle.attention(q, k, v2, 0.4)
+    o12, _, _ = oracle.attention(q, k, 2.0 * v1 - 3.0 * v2, 0.4)
+    assert np.max(np.abs(o12 - (2.0 * o1 - 3.0 * o2))) <= 1e-13
+
+
+def test_one_hot_dominant_logit_selects_its_value_row():
+    rng = np.random.default_rng(12)
+    Lk, D = 20, 8
+    k = rng.standard_normal((1, 1, Lk, D)) * 0.1
+    v = rng.standard_normal((1, 1, Lk, D))
+    star = 13
+    k[0, 0, star, 0] = 10.0
+    q = np.zeros((1, 1, 3, D))
+    q[0, 0, :, 0] = 6.0        # logit gap >= 6*(10 - 0.5) = 57 > 40
+    o, L, S = oracle.attention(q, k, v, 1.0)
+    assert np.max(np.abs(o[0, 0] - v[0, 0, star])) <= 1e-15 * 1e3
+    assert np.allclose(L, 60.0) and np.all(np.abs(S - 1.0) < 1e-16 * 1e3)
+
+
+# ------------------------------------------------------ Eq. 4 and its merge
+
+def test_softmax_rows_probabilities_sum_to_one():
+    a = wl.make_matrix(33, 517, seed=13, dtype="f16", sigma=3.0)
+    L, S, P = oracle.softmax_rows(a, scale=0.7, want_p=True)
+    assert np.max(np.abs(P.sum(axis=1) - 1.0)) <= 1e-13
+    assert np.all(P >= 0) and np.all(P <= 1.0)
+    # the max element has weight exactly 1/S
+    am = float(np.float32(0.7)) * a.astype(np.float64)   # the scale the GPU receives is fp32
+    assert np.array_equal(L, am.max(axis=1))
+    assert np.allclose(P[np.arange(33), am.argmax(axis=1)], 1.0 / S, rtol=1e-15)
+
+
+def test_softmax_rows_shift_invariance():
+    rng = np.random.default_rng(14)
+    a = rng.standard_normal((12, 64))
+    c = rng.integers(-50, 50, size=(12, 1)).astype(np.float64)
+    L1, S1, P1 = oracle.softmax_rows(a, want_p=True)
+    L2, S2, P2 = oracle.softmax_rows(a + c, want_p=True)
+    assert np.max(np.abs(L2 - (L1 + c[:, 0]))) <= 1e-13
+    assert np.max(np.abs(S2 - S1) / S1) <= 1e-12
+    assert np.max(np.abs(P2 - P1)) <= 1e-12
+
+
+def _merge(m1, s1, m2, s2):
+    """Combine two blocks' (max, shifted sum) pairs: the multi-stage reduction."""
+    M = np.maximum(m1, m2)
+    return M, s1 * np.exp(m1 - M) + s2 * np.exp(m2 - M)
+
+
+def test_block_merge_rule_reproduces_whole_row_statistics():
+    rng = np.random.default_rng(15)
+    a = rng.standard_normal((40, 300)) * 4.0
+    L, S = oracle.softmax_rows(a)
+    for _ in range(5):
+        cut = int(rng.integers(1, 299))
+        L1, S1 = oracle.softmax_rows(np.ascontiguousarray(a[:, :cut]))
+        L2, S2 = oracle.softmax_rows(np.ascontiguousarray(a[:, cut:]))
+        M, T = _merge(L1, S1, L2, S2)
+        assert np.array_equal(M, L)
+        assert np.max(np.abs(T - S) / S) <= 1e-13
+    # four-way, merged in two different orders
+    parts = np.array_split(np.arange(300), 4)
+    st = [oracle.softmax_rows(np.ascontiguousarray(a[:, p])) for p in parts]
+    left = _merge(*_merge(*st[0], *st[1]), *_merge(*st[2], *st[3]))
+    right = _merge(*st[0], *_merge(*st[1], *_merge(*st[2], *st[3])))
+    for m, s in (left, right):
+        assert np.array_equal(m, L)
+        assert np.max(np.abs(s - S) / S) <= 1e-13
+
+
+def test_softmax_rows_matches_torch_logsumexp():
+    torch = pytest.importorskip("torch")
+    a = wl.make_matrix(20, 1000, seed=16, dtype="f32", sigma=5.0)
+    L, S, P = oracle.softmax_rows(a, scale=0.5, want_p=True)
+    t = torch.from_numpy(a.astype(np.float64)) * float(np.float32(0.5))
+    assert np.array_equal(L, t.max(dim=1).values.numpy())
+    lse = torch.logsumexp(t, dim=1).numpy()
+    assert np.max(np.abs(np.log(S) + L - lse)) <= 1e-12
+    assert np.max(np.abs(P - torch.softmax(t, dim=1).numpy())) <= 1e-15
+
+
+# ----------------------------------- independent library at workload shapes
+
+def _torch_sdpa_rows(q, k, v, scale, rows):
+    torch = pytest.importorskip("torch")
+    B, H, Lq, D = q.shape
+    qq = torch.from_numpy(q.astype(np.float64)).reshape(B * H, Lq, D)
+    kk = torch.from_numpy(k.astype(np.float64)).reshape(B * H, -1, D)
+    vv = torch.from_numpy(v.astype(np.float64)).reshape(B * H, -1, D)
+    out = np.empty((rows.size, D))
+    bh = rows // Lq
+    for g in np.unique(bh):
+        sel = np.nonzero(bh == g)[0]
+        qi = qq[g, rows[sel] % Lq][None]
+        o = torch.nn.functional.scaled_dot_product_attention(qi, kk[g][None], vv[g][None],
+                                                             scale=float(np.float32(scale)))
+        out[sel] = o[0].numpy()
+    return out
+
+
+@pytest.mark.parametrize("name", ["mid8_self", "mid8_cross", "l16_self_peaked", "l16_cross",
+                                  "l32_self", "l32_cross", "l64_self", "l64_cross"])
+def test_matches_torch_fp64_sdpa_at_unet_shapes(name):
+    case = wl.CASES[name]
+    q, k, v = wl.case_inputs(case)
+    per_head = case.Lq if case.Lq <= 256 else 8
+    rows = wl.sample_rows(case.B, case.H, case.Lq, per_head, seed=case.seed)
+    o, _, _ = oracle.attention(q, k, v, case.scale, rows=rows)
+    ref = _torch_sdpa_rows(q, k, v, case.scale, rows)
+    assert np.max(np.abs(o - ref)) <= 1e-12
+
+
+def test_rejects_bad_arguments():
+    q = np.zeros((1, 1, 2, 8), np.float16)
+    with pytest.raises(ValueError):
+        oracle.attention(q, np.zeros((1, 1, 3, 8), np.float16), np.zeros((1, 1, 4, 8), np.float16), 1.0)
+    with pytest.raises(ValueError):
+        oracle.attention(q, q, q, 1.0, rows=np.array([2]))
+    with pytest.raises(ValueError):
+        oracle.softmax_rows(np.zeros((0, 4), np.float32))
+
+
+# ------------------------------------------------------ the input generator
+
+def test_generator_is_seeded_and_shaped():
+    c = wl.CASES["l32_cross"]
+    q1, k1, v1 = wl.case_inputs(c)
+    q2, k2, v2 = wl.case_inputs(c)
+    assert q1.shape == (2, 8, 1024, 80) and k1.shape == (2, 8, 77, 80) and v1.shape == k1.shape
+    assert q1.dtype == np.float16
+    assert np.array_equal(q1, q2) and np.array_equal(k1, k2) and np.array_equal(v1, v2)
+    assert abs(float(q1.astype(np.float64).std()) - 1.0) < 0.01
+    peaked = wl.case_inputs(wl.CASES["l16_self_peaked"])[0]
+    plain = wl.case_inputs(wl.CASES["l16_self"])[0]
+    assert np.array_equal(peaked.astype(np.float64), 4.0 * plain.astype(np.float64))
+
+
+def test_bf16_rounding_matches_torch():
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(17)
+    x = rng.standard_normal(50000, dtype=np.float32) * 3
+    ours = wl.to_bf16_bits(x)
+    ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(ours, ref)
+
+
+def test_sweep_has_sixteen_blocks_of_self_and_cross():
+    cases = wl.sweep_cases(0)
+    assert len(cases) == 32
+    sides = [c.Lq for c in cases[::2]]
+    assert sides == [4096] * 2 + [1024] * 2 + [256] * 2 + [64] + [256] * 3 + [1024] * 3 + [4096] * 3
+    assert all(c.Lk == 77 for c in cases[1::2])
+    assert len({c.seed for s in range(20) for c in wl.sweep_cases(s)}) == 640

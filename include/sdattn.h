@@ -1,0 +1,115 @@
+/*
+ * sdattn.h -- C ABI of libsdattn, the attention of Stable Diffusion 1.4's
+ * UNet transformer blocks as hand-written HIP kernels for AMD MI355X (gfx950).
+ *
+ * The operation is the one stated in Sec. 3.2.1 ("Partially Fused Softmax")
+ * of "Speed Is All You Need: On-Device Acceleration of Large Diffusion Models
+ * via GPU-Aware Optimizations" (Chen et al., 2023):
+ *
+ *   Eq. 3   Attention(Q, K, V) = softmax(Q K^T / sqrt(d)) V,
+ *           Q in R^{N x d}, K, V in R^{M x d}
+ *   Eq. 4   L = [max_j a_ij],  S = [sum_j exp(a_ij - max_k a_ik)]   for A = Q K^T / sqrt(d)
+ *
+ * followed by the element-wise normalisation exp(a_ij - L_i) / S_i.  Here N is
+ * Lq (latent tokens), M is Lk (latent tokens for self-attention, text tokens
+ * for cross-attention) and d is D, applied independently to each of B*H
+ * (batch, head) pairs.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Memory.    Every tensor argument is a device pointer owned by the caller.
+ *            The library allocates nothing, frees nothing and keeps no state
+ *            beyond a thread-local copy of the last HIP error.
+ * Layout.    Dense row-major, innermost dimension last, no strides.
+ * Streams.   `stream` is a hipStream_t (NULL = the default stream).  Work is
+ *            enqueued on it and the call returns at once; a fault on the
+ *            device shows up at the caller's next synchronisation.
+ * Errors.    Arguments are checked before anything is enqueued.  On any
+ *            nonzero status nothing was launched and no output was written.
+ * Values.    Inputs are not scanned: NaN or Inf inputs give unspecified
+ *            (NaN/Inf) outputs.
+ * Rounding.  fp16/bf16 inputs, fp32 accumulation, probabilities rounded to
+ *            the input type before the product with V, outputs rounded to
+ *            nearest even.
+ */
+#ifndef SDATTN_H
+#define SDATTN_H
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    SDATTN_OK = 0,
+    SDATTN_ERR_INVALID_ARG = 1,  /* NULL pointer, size < 1, non-finite scale, overlap, bad dtype */
+    SDATTN_ERR_UNSUPPORTED = 2,  /* D not a multiple of 8, D > 256, or a grid too large */
+    SDATTN_ERR_MISALIGNED = 3,   /* a pointer is not aligned as documented */
+    SDATTN_ERR_HIP = 4           /* a HIP runtime call failed; see sdattn_last_hip_error() */
+} sdattn_status;
+
+typedef enum {
+    SDATTN_F16 = 0,              /* IEEE binary16 */
+    SDATTN_BF16 = 1,             /* bfloat16 */
+    SDATTN_F32 = 2               /* IEEE binary32 (sdattn_softmax_rows input only) */
+} sdattn_dtype;
+
+/*
+ * Eq. 3 for fp16 tensors.
+ *
+ *   q   [B, H, Lq, D] fp16     queries
+ *   k   [B, H, Lk, D] fp16     keys
+ *   v   [B, H, Lk, D] fp16     values
+ *   out [B, H, Lq, D] fp16     out[b,h,i,:] = sum_j softmax_j(scale * q_i . k_j) v_j
+ *
+ * scale multiplies every logit; SD uses 1/sqrt(D) with the true head width
+ * (any finite value is accepted, including 0 and negative values).
+ * Requirements: q, k, v, out 16-byte aligned; B, H, Lq, Lk >= 1;
+ * 8 <= D <= 256 with D % 8 == 0; out must not overlap q, k or v.
+ * Returns an sdattn_status.
+ */
+int sdattn_forward(const void *q, const void *k, const void *v, void *out,
+                   int B, int H, int Lq, int Lk, int D, float scale, void *stream);
+
+/*
+ * sdattn_forward for fp16 or bf16 (`dtype`, all four tensors alike), with an
+ * optional per-row output of Eq. 4's statistics:
+ *
+ *   ls  NULL, or fp32 [B, H, Lq, 2]: ls[..., 0] = L_i = max_j scale * q_i . k_j,
+ *       ls[..., 1] = S_i = sum_j exp(scale * q_i . k_j - L_i) (S_i >= 1).
+ *       8-byte aligned, must not overlap any other argument.
+ *
+ * SDATTN_F32 is rejected with SDATTN_ERR_UNSUPPORTED.
+ */
+int sdattn_forward_ex(const void *q, const void *k, const void *v, void *out, float *ls,
+                      int B, int H, int Lq, int Lk, int D, float scale,
+                      sdattn_dtype dtype, void *stream);
+
+/*
+ * The reduction step of Eq. 4 (and, optionally, the element-wise step) on a
+ * given matrix, as one kernel launch with a multi-stage (block-wise) reduction
+ * of each row (Sec. 3.2.1, the paragraph after Eq. 4).
+ *
+ *   a   [rows, cols] of `dtype` (fp16, bf16 or fp32), with a_rj = scale * a[r, j]
+ *   ls  fp32 [rows, 2]: ls[r, 0] = L_r = max_j a_rj, ls[r, 1] = S_r = sum_j exp(a_rj - L_r)
+ *   p   NULL, or [rows, cols] of `dtype`: p[r, j] = exp(a_rj - L_r) / S_r
+ *
+ * Requirements: a and p 16-byte aligned, ls 8-byte aligned; rows, cols >= 1;
+ * rows * cols < 2^62; no output may overlap another argument; finite scale.
+ */
+int sdattn_softmax_rows(const void *a, float *ls, void *p, long long rows, long long cols,
+                        float scale, sdattn_dtype dtype, void *stream);
+
+/* Static English text for a status code (never NULL). */
+const char *sdattn_status_str(int status);
+
+/* hipError_t of the last failed HIP call on this thread (0 if none). */
+int sdattn_last_hip_error(void);
+
+/* Static version string of the library. */
+const char *sdattn_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SDATTN_H */

@@ -1,0 +1,36 @@
+// launch.h -- host-side launchers of the sdattn kernels (internal to the library).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+namespace sdattn {
+
+struct AttnArgs {
+    const void* q;
+    const void* k;
+    const void* v;
+    void* out;
+    float* ls;      // optional [B,H,Lq,2] (L, S), may be null
+    int B, H, Lq, Lk, D;
+    float scale;
+    int dtype;      // ElemType: kF16 or kBF16
+    void* stream;
+};
+
+// Number of workgroups the attention kernel launches for these sizes.
+long long attn_fwd_grid(int B, int H, int Lq);
+hipError_t launch_attn_fwd(const AttnArgs& a);
+
+struct SoftmaxArgs {
+    const void* a;
+    float* ls;      // [rows, 2]
+    void* p;        // optional [rows, cols], may be null
+    long long rows, cols;
+    float scale;
+    int dtype;      // ElemType: kF16, kBF16 or kF32
+    void* stream;
+};
+
+hipError_t launch_softmax_rows(const SoftmaxArgs& a);
+
+}  // namespace sdattn

@@ -1,0 +1,143 @@
+"""The C ABI on the host: the library loads, exports what include/sdattn.h
+declares, and rejects bad arguments with the documented status before any
+HIP call (so these run without a GPU; the pointers are never dereferenced).
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2304_11267_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sdattn.h")
+
+OK, INVALID, UNSUPPORTED, MISALIGNED, HIPERR = 0, 1, 2, 3, 4
+F16, BF16, F32 = 0, 1, 2
+
+# fake, well-aligned, non-overlapping device addresses (never touched)
+QA, KA, VA, OA, LA = (ctypes.c_void_p(x) for x in (0x10000000, 0x20000000, 0x30000000,
+                                                   0x40000000, 0x50000000))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(binding.library_path()):
+        pytest.skip("libsdattn.so not built")
+    return binding.load_library()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sdattn_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_binding_exports():
+    assert declared_functions() == sorted(binding.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings(lib):
+    for code in (OK, INVALID, UNSUPPORTED, MISALIGNED, HIPERR, 99, -1):
+        s = lib.sdattn_status_str(code)
+        assert isinstance(s, bytes) and len(s) > 0
+    assert lib.sdattn_status_str(OK) == b"ok"
+    assert lib.sdattn_status_str(99) == b"unknown status"
+    assert lib.sdattn_last_hip_error() == 0
+    assert b"gfx950" in lib.sdattn_version()
+
+
+def fwd(lib, q=QA, k=KA, v=VA, o=OA, B=2, H=8, Lq=64, Lk=77, D=40, scale=0.158):
+    return lib.sdattn_forward(q, k, v, o, B, H, Lq, Lk, D, ctypes.c_float(scale), None)
+
+
+def fwd_ex(lib, ls=None, dtype=F16, **kw):
+    a = dict(q=QA, k=KA, v=VA, o=OA, B=2, H=8, Lq=64, Lk=77, D=40, scale=0.158)
+    a.update(kw)
+    return lib.sdattn_forward_ex(a["q"], a["k"], a["v"], a["o"], ls, a["B"], a["H"], a["Lq"],
+                                 a["Lk"], a["D"], ctypes.c_float(a["scale"]), dtype, None)
+
+
+@pytest.mark.parametrize("field", ["q", "k", "v", "o"])
+def test_null_pointer_is_invalid(lib, field):
+    assert fwd(lib, **{field: None}) == INVALID
+
+
+@pytest.mark.parametrize("field", ["B", "H", "Lq", "Lk", "D"])
+@pytest.mark.parametrize("value", [0, -3])
+def test_nonpositive_sizes_are_invalid(lib, field, value):
+    assert fwd(lib, **{field: value}) == INVALID
+
+
+@pytest.mark.parametrize("scale", [float("inf"), float("-inf"), float("nan")])
+def test_nonfinite_scale_is_invalid(lib, scale):
+    assert fwd(lib, scale=scale) == INVALID
+
+
+@pytest.mark.parametrize("D", [4, 12, 41, 264, 512])
+def test_unsupported_head_width(lib, D):
+    assert fwd(lib, D=D) == UNSUPPORTED
+
+
+def test_oversized_problem_is_unsupported(lib):
+    assert fwd(lib, B=1 << 20, H=1 << 20, Lq=1 << 20, D=8) == UNSUPPORTED
+
+
+@pytest.mark.parametrize("field", ["q", "k", "v", "o"])
+def test_misaligned_pointer(lib, field):
+    base = {"q": 0x10000000, "k": 0x20000000, "v": 0x30000000, "o": 0x40000000}[field]
+    assert fwd(lib, **{field: ctypes.c_void_p(base + 8)}) == MISALIGNED
+
+
+def test_output_overlapping_an_input_is_invalid(lib):
+    # q spans 2*8*64*40*2 bytes from QA; put out inside it
+    assert fwd(lib, o=ctypes.c_void_p(0x10000000 + 4096)) == INVALID
+    assert fwd(lib, o=KA) == INVALID
+    assert fwd(lib, o=ctypes.c_void_p(0x30000000 - 16)) == INVALID   # out's tail runs into v
+
+
+def test_forward_ex_checks(lib):
+    assert fwd_ex(lib, dtype=F32) == UNSUPPORTED
+    assert fwd_ex(lib, dtype=7) == INVALID
+    assert fwd_ex(lib, ls=ctypes.c_void_p(0x50000004)) == MISALIGNED
+    assert fwd_ex(lib, ls=ctypes.c_void_p(0x40000000 + 64)) == INVALID   # ls inside out
+    assert fwd_ex(lib, dtype=BF16, D=44) == UNSUPPORTED
+
+
+def sm(lib, a=QA, ls=LA, p=None, rows=16, cols=4096, scale=1.0, dtype=F16):
+    return lib.sdattn_softmax_rows(a, ls, p, rows, cols, ctypes.c_float(scale), dtype, None)
+
+
+def test_softmax_rows_checks(lib):
+    assert sm(lib, a=None) == INVALID
+    assert sm(lib, ls=None) == INVALID
+    assert sm(lib, rows=0) == INVALID
+    assert sm(lib, cols=-1) == INVALID
+    assert sm(lib, scale=float("nan")) == INVALID
+    assert sm(lib, dtype=9) == INVALID
+    assert sm(lib, rows=1 << 40, cols=1 << 30) == UNSUPPORTED
+    assert sm(lib, a=ctypes.c_void_p(0x10000002)) == MISALIGNED
+    assert sm(lib, p=ctypes.c_void_p(0x30000008)) == MISALIGNED
+    assert sm(lib, ls=ctypes.c_void_p(0x50000004)) == MISALIGNED
+    assert sm(lib, ls=ctypes.c_void_p(0x10000000 + 1024)) == INVALID    # ls inside a
+    assert sm(lib, p=ctypes.c_void_p(0x10000000 + 4096)) == INVALID     # p overlaps a
+    assert sm(lib, p=ctypes.c_void_p(0x50000000 - 64)) == INVALID       # p overlaps ls
+
+
+def test_rejected_calls_leave_no_hip_error(lib):
+    fwd(lib, q=None)
+    sm(lib, a=None)
+    assert lib.sdattn_last_hip_error() == 0
+
+
+def test_binding_raises_when_library_missing(monkeypatch, tmp_path):
+    monkeypatch.setattr(binding, "_lib", None)
+    monkeypatch.setenv("SDATTN_LIBRARY", str(tmp_path / "absent.so"))
+    with pytest.raises(RuntimeError, match="not built"):
+        binding.load_library()

@@ -1,0 +1,244 @@
+"""GPU parity of the HIP attention path against the fp64 oracle.
+
+Every call goes through the C ABI (libsdattn.so) via the thin binding; the
+reference is the oracle on the same seeded inputs.  Sizes span several
+128-row query tiles and 64-key tiles with ragged tails; the UNet shapes run
+at full size (sampled rows where the oracle would be slow), in the launch
+configuration the benchmark times.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2304_11267_amd as sd
+from paper_2304_11267_amd import workloads as wl
+
+from parity_util import assert_close, to_device, to_host64
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _needs_gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    sd.load_library()
+
+
+def run_forward(q, k, v, scale, dtype="f16", want_ls=False):
+    import torch
+    qd, kd, vd = (to_device(t, dtype) for t in (q, k, v))
+    out = torch.empty_like(qd)
+    ls = None
+    if want_ls:
+        ls = torch.empty(qd.shape[:3] + (2,), dtype=torch.float32, device=qd.device)
+    if dtype == "f16" and not want_ls:
+        sd.forward(qd, kd, vd, out, scale)
+    else:
+        sd.forward_ex(qd, kd, vd, out, scale, ls=ls)
+    torch.cuda.synchronize()
+    o = to_host64(out)
+    return (o, ls.cpu().numpy().astype(np.float64)) if want_ls else o
+
+
+def check_case(q, k, v, scale, dtype="f16", rows=None, what=""):
+    g, ls = run_forward(q, k, v, scale, dtype, want_ls=True)
+    r, L, S = oracle.attention(q, k, v, scale, rows=rows, dtype="bf16" if dtype == "bf16" else None)
+    D = q.shape[3]
+    if rows is not None:
+        g = g.reshape(-1, D)[rows]
+        ls = ls.reshape(-1, 2)[rows]
+    else:
+        ls = ls.reshape(L.shape + (2,))
+    assert_close(g, r, dtype, what)
+    # Eq. 4's statistics: L to fp32 rounding of the logits, S to the rounding of p
+    assert np.max(np.abs(ls[..., 0] - L) / np.maximum(1.0, np.abs(L))) <= 1e-5, what
+    srel = 2e-3 if dtype == "f16" else 1e-2
+    assert np.max(np.abs(ls[..., 1] - S) / S) <= srel, what
+
+
+@pytest.mark.parametrize("name", ["mid8_self", "mid8_cross", "l16_self", "l16_self_peaked",
+                                  "l16_cross", "l32_cross", "l64_cross"])
+def test_unet_case_full(name):
+    case = wl.CASES[name]
+    q, k, v = wl.case_inputs(case)
+    check_case(q, k, v, case.scale, what=name)
+
+
+@pytest.mark.parametrize("name,per_head", [("l32_self", 96), ("l64_self", 48)])
+def test_unet_case_sampled_rows(name, per_head):
+    case = wl.CASES[name]
+    q, k, v = wl.case_inputs(case)
+    rows = wl.sample_rows(case.B, case.H, case.Lq, per_head, seed=case.seed + 5)
+    check_case(q, k, v, case.scale, rows=rows, what=name)
+
+
+@pytest.mark.parametrize("name", ["mid8_self", "l16_self_peaked", "l32_cross"])
+def test_unet_case_bf16(name):
+    case = wl.CASES[name]
+    q, k, v = wl.case_inputs(case, dtype="bf16")
+    check_case(q, k, v, case.scale, dtype="bf16", what=name + "/bf16")
+
+
+RAGGED = [
+    # (B, H, Lq, Lk, D)
+    (1, 1, 1, 1, 40),
+    (1, 2, 5, 3, 8),
+    (2, 1, 100, 65, 16),
+    (1, 3, 129, 63, 24),
+    (2, 2, 130, 129, 32),
+    (1, 1, 257, 200, 48),
+    (1, 2, 64, 77, 64),
+    (2, 1, 200, 300, 80),
+    (1, 1, 131, 127, 96),
+    (1, 1, 70, 191, 128),
+    (1, 1, 33, 77, 160),
+    (1, 1, 40, 70, 200),
+    (1, 1, 40, 65, 256),
+]
+
+
+@pytest.mark.parametrize("shape", RAGGED, ids=lambda s: "x".join(map(str, s)))
+def test_ragged_shapes(shape):
+    B, H, Lq, Lk, D = shape
+    seed = 77 + Lq * 3 + Lk * 5 + D
+    q, k, v = wl.make_qkv(B, H, Lq, Lk, D, seed)
+    check_case(q, k, v, float(np.float32(1 / np.sqrt(D))), what=str(shape))
+
+
+@pytest.mark.parametrize("scale", [0.0, -0.2, 1.0])
+def test_scale_values(scale):
+    q, k, v = wl.make_qkv(1, 2, 70, 90, 40, 901)
+    check_case(q, k, v, scale, what=f"scale={scale}")
+
+
+def test_constant_keys_give_mean_of_values():
+    q, k, v = wl.make_qkv(1, 2, 130, 100, 40, 902)
+    k[:] = k[:, :, :1]
+    g = run_forward(q, k, v, 0.158)
+    ref = np.broadcast_to(v.astype(np.float64).mean(axis=2, keepdims=True), g.shape)
+    assert_close(g, ref, what="constant K")
+
+
+def test_single_key_returns_value():
+    q, k, v = wl.make_qkv(2, 2, 100, 1, 80, 903)
+    g = run_forward(q, k, v, 0.11)
+    assert np.array_equal(g, np.broadcast_to(v.astype(np.float64), g.shape))
+
+
+def test_one_hot_dominant_logit():
+    B, H, Lq, Lk, D = 1, 1, 64, 77, 40
+    q = np.zeros((B, H, Lq, D), np.float16)
+    k = (np.random.default_rng(904).standard_normal((B, H, Lk, D)) * 0.05).astype(np.float16)
+    v = np.random.default_rng(905).standard_normal((B, H, Lk, D)).astype(np.float16)
+    star = np.arange(Lq) % Lk
+    # query i points at key star[i] through its own coordinate d = i % D
+    for i in range(Lq):
+        q[0, 0, i, i % D] = 8.0
+    for j in range(Lk):
+        k[0, 0, j, j % D] = 8.0
+    # logits: 64*scale for the matching key(s) vs < 1 otherwise; several keys share i % D
+    g = run_forward(q, k, v, 1.0)
+    r, _, _ = oracle.attention(q, k, v, 1.0)
+    assert_close(g, r, what="one-hot")
+    lone = [i for i in range(Lq) if sum(1 for j in range(Lk) if j % D == i % D) == 1]
+    for i in lone:
+        assert np.max(np.abs(g[0, 0, i] - v[0, 0, i % D].astype(np.float64))) <= 2e-3
+
+
+def test_joint_permutation_invariance_on_gpu():
+    q, k, v = wl.make_qkv(1, 2, 128, 77, 40, 906)
+    perm = np.random.default_rng(907).permutation(77)
+    g1 = run_forward(q, k, v, 0.158)
+    g2 = run_forward(q, k[:, :, perm].copy(), v[:, :, perm].copy(), 0.158)
+    assert np.max(np.abs(g1 - g2)) <= 2e-3
+
+
+def test_bitwise_deterministic():
+    q, k, v = wl.make_qkv(2, 8, 1024, 1024, 40, 908)
+    outs = [run_forward(q, k, v, 0.158) for _ in range(3)]
+    assert np.array_equal(outs[0], outs[1]) and np.array_equal(outs[0], outs[2])
+
+
+def test_inputs_may_alias():
+    import torch
+    q, _, _ = wl.make_qkv(1, 2, 96, 96, 40, 909)
+    qd = to_device(q)
+    out = torch.empty_like(qd)
+    sd.forward(qd, qd, qd, out, 0.158)
+    torch.cuda.synchronize()
+    r, _, _ = oracle.attention(q, q, q, 0.158)
+    assert_close(to_host64(out), r, what="q=k=v")
+
+
+def test_bad_arguments_raise():
+    import torch
+    q = torch.zeros(1, 1, 8, 12, dtype=torch.float16, device="cuda")
+    with pytest.raises(sd.SdattnError) as e:
+        sd.forward(q, q, q, torch.empty_like(q), 1.0)
+    assert e.value.status == sd.STATUS_UNSUPPORTED
+
+
+@pytest.mark.parametrize("step", [0, 19])
+def test_sweep_step_sampled(step):
+    """One UNet evaluation (16 blocks, self then cross) at a denoising step."""
+    for case in wl.sweep_cases(step):
+        q, k, v = wl.case_inputs(case)
+        rows = wl.sample_rows(case.B, case.H, case.Lq, 8, seed=case.seed)
+        check_case(q, k, v, case.scale, rows=rows, what=case.name)
+
+
+# ------------------------------------------------------------ softmax_rows
+
+def run_softmax_rows(a, scale, dtype, want_p):
+    import torch
+    ad = to_device(a, "bf16" if dtype == "bf16" else None)
+    rows, cols = a.shape
+    ls = torch.empty(rows, 2, dtype=torch.float32, device="cuda")
+    p = torch.empty_like(ad) if want_p else None
+    sd.softmax_rows(ad, ls, p, scale=scale)
+    torch.cuda.synchronize()
+    return ls.cpu().numpy().astype(np.float64), (to_host64(p) if want_p else None)
+
+
+@pytest.mark.parametrize("rows,cols,dtype", [
+    (64, 4096, "f16"), (7, 77, "f16"), (33, 1000, "f32"), (5, 13, "f32"),
+    (16, 20000, "f16"), (3, 50001, "f32"), (100, 256, "bf16"), (1, 1, "f16"),
+])
+def test_softmax_rows_matches_oracle(rows, cols, dtype):
+    a = wl.make_matrix(rows, cols, seed=rows * 7 + cols, dtype=dtype, sigma=4.0)
+    scale = 0.7
+    ls, p = run_softmax_rows(a, scale, dtype, want_p=True)
+    L, S, P = oracle.softmax_rows(a, scale=scale, want_p=True, dtype="bf16" if dtype == "bf16" else None)
+    assert np.max(np.abs(ls[:, 0] - L) / np.maximum(1.0, np.abs(L))) <= 1e-6
+    assert np.max(np.abs(ls[:, 1] - S) / S) <= 1e-4
+    # fp32: the exponent argument a - L (up to ~25 in log2 units here) carries
+    # fp32 rounding of ~25 * 2^-23, i.e. ~2.5e-6 relative in p; fp16 / bf16 add
+    # the rounding of p itself (2^-11 / 2^-8), measured above fp16's subnormal range.
+    ptol = {"f32": 1e-5, "f16": 1e-3, "bf16": 8e-3}[dtype]
+    prel = float(np.max(np.abs(p - P) / np.maximum(P, 1e-30 if dtype == "f32" else 6e-5)))
+    assert prel <= ptol, f"p relative error {prel:.3e} > {ptol}"
+    psum = float(np.max(np.abs(p.sum(axis=1) - 1.0)))
+    assert psum <= {"f32": 1e-5, "f16": 2e-3, "bf16": 1.6e-2}[dtype], f"rows of p sum to 1 +- {psum:.3e}"
+
+
+def test_softmax_rows_without_p_and_negative_scale():
+    a = wl.make_matrix(40, 4096, seed=11, dtype="f16")
+    ls, _ = run_softmax_rows(a, -1.5, "f16", want_p=False)
+    L, S = oracle.softmax_rows(a, scale=-1.5)
+    assert np.max(np.abs(ls[:, 0] - L) / np.maximum(1.0, np.abs(L))) <= 1e-6
+    assert np.max(np.abs(ls[:, 1] - S) / S) <= 1e-4
+
+
+def test_softmax_rows_on_attention_logits_matches_forward_stats():
+    """softmax_rows on A = Q K^T reproduces the (L, S) the fused forward reports."""
+    import torch
+    q, k, v = wl.make_qkv(1, 2, 256, 256, 40, 910)
+    scale = 0.158
+    a = np.einsum("bhid,bhjd->bhij", q.astype(np.float64), k.astype(np.float64)).reshape(-1, 256)
+    ls_rows, _ = run_softmax_rows(a.astype(np.float32), scale, "f32", want_p=False)
+    _, ls_fwd = run_forward(q, k, v, scale, want_ls=True)
+    ls_fwd = ls_fwd.reshape(-1, 2)
+    assert np.max(np.abs(ls_rows[:, 0] - ls_fwd[:, 0])) <= 1e-5 * np.abs(ls_rows[:, 0]).max()
+    assert np.max(np.abs(ls_rows[:, 1] - ls_fwd[:, 1]) / ls_rows[:, 1]) <= 2e-3

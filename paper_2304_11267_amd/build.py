@@ -17,7 +17,7 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libsdattn.so")
 ARCH = "gfx950"
 
-SOURCES = ["attn_fwd.hip", "softmax_rows.hip", "sdattn_api.hip"]
+SOURCES = ["attn_fwd.hip", "attn_fwd_generic.hip", "softmax_rows.hip", "sdattn_api.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 CFLAGS = [
@@ -26,6 +26,9 @@ CFLAGS = [
     "-I", os.path.join(ROOT, "include"), "-I", CSRC,
     # keep the compiler from emitting packed fp32 ops (v_pk_fma_f32 and friends)
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # matrix-core results in ordinary VGPRs: the softmax reads them directly
+    # instead of copying them out of accumulation registers
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
 ]
 
 

@@ -7,6 +7,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+#include <utility>
+
 namespace sdattn {
 
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
@@ -36,14 +39,17 @@ __device__ __forceinline__ f32x16 mfma32x32x16(u32x4 a, u32x4 b, f32x16 c) {
 }
 
 // Round two floats to the 16-bit type (nearest even) and pack them, x in the low half.
+// (one v_cvt_pk_f16_f32 / v_cvt_pk_bf16_f32)
 template <int ET>
 __device__ __forceinline__ uint32_t pack2(float x, float y) {
+    typedef float f2 __attribute__((ext_vector_type(2)));
+    const f2 v = {x, y};
     if constexpr (ET == kF16) {
-        _Float16 a = (_Float16)x, b = (_Float16)y;
-        return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+        typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+        return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, h2));
     } else {
-        __bf16 a = (__bf16)x, b = (__bf16)y;
-        return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+        typedef __bf16 b2 __attribute__((ext_vector_type(2)));
+        return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, b2));
     }
 }
 

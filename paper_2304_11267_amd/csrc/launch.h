@@ -17,9 +17,12 @@ struct AttnArgs {
     void* stream;
 };
 
-// Number of workgroups the attention kernel launches for these sizes.
+// Number of workgroups the attention kernels launch for these sizes.
 long long attn_fwd_grid(int B, int H, int Lq);
+// Picks the kernel for (D, Lk) and launches it.
 hipError_t launch_attn_fwd(const AttnArgs& a);
+// The generic kernel (any D % 8 == 0 up to 256).
+hipError_t launch_attn_fwd_generic(const AttnArgs& a);
 
 struct SoftmaxArgs {
     const void* a;

@@ -43,8 +43,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing")
     ap.add_argument("--no-extras", action="store_true",
                     help="time only the step (no cold cross or softmax_rows legs)")
-    ap.add_argument("--cpu-rows-per-head", type=int, default=384,
+    ap.add_argument("--cpu-rows-per-head", type=int, default=2560,
                     help="self-attention rows per (b, h) the oracle times")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain 256 MiB device copy (scales the HBM traffic counters)")
     return ap.parse_args()
 
 
@@ -149,6 +151,9 @@ def main():
         out["cross"].update(cold_cross(torch, sd, wl, dev, stream, cross_case))
         out["softmax_rows"] = bench_softmax_rows(torch, sd, dev, stream)
 
+    if args.copy_calibration:
+        out["copy_calibration"] = copy_calibration(torch, dev, stream)
+
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, self_case, cross_case, args.cpu_rows_per_head)
 
@@ -207,6 +212,23 @@ def bench_softmax_rows(torch, sd, dev, stream, reps=10):
     return res
 
 
+def copy_calibration(torch, dev, stream, nbytes=256 << 20, reps=3):
+    """A plain device copy of known size: its FETCH_SIZE / WRITE_SIZE counter
+    readings give the scale between those counters and bytes moved."""
+    src = torch.ones(nbytes // 2, dtype=torch.float16, device=dev)
+    dst = torch.empty_like(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    dst.copy_(src)
+    e0.record(stream)
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    return {"bytes_read": nbytes, "bytes_written": nbytes, "avg_kernel_us": round(ms * 1e3, 2),
+            "gbs": round(2 * nbytes / (ms * 1e-3) / 1e9, 1)}
+
+
 def cpu_baseline(wl, self_case, cross_case, rows_per_head):
     import oracle
     q, k, v = wl.case_inputs(self_case)
@@ -215,7 +237,7 @@ def cpu_baseline(wl, self_case, cross_case, rows_per_head):
     oracle.attention(q, k, v, self_case.scale, rows=rows)
     t_self = time.perf_counter() - t0
     cq, ck, cv = wl.case_inputs(cross_case)
-    crows = wl.sample_rows(cross_case.B, cross_case.H, cross_case.Lq, rows_per_head, seed=2)
+    crows = wl.sample_rows(cross_case.B, cross_case.H, cross_case.Lq, cross_case.Lq, seed=2)
     t0 = time.perf_counter()
     oracle.attention(cq, ck, cv, cross_case.scale, rows=crows)
     t_cross = time.perf_counter() - t0

@@ -464,6 +464,7 @@ long long attn_fwd_grid(int B, int H, int Lq) {
 }
 
 hipError_t launch_attn_fwd(const AttnArgs& a) {
+    if (attn_fwd_short_supported(a.D, a.Lk)) return launch_attn_fwd_short(a);
     if (a.D < 32) return launch_attn_fwd_generic(a);
     using Seq = std::make_integer_sequence<int, 32>;   // D = 8, 16, ..., 256
     return a.dtype == kF16 ? dispatch_d<kF16>(a, Seq{}) : dispatch_d<kBF16>(a, Seq{});

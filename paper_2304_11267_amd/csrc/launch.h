@@ -23,6 +23,9 @@ long long attn_fwd_grid(int B, int H, int Lq);
 hipError_t launch_attn_fwd(const AttnArgs& a);
 // The generic kernel (any D % 8 == 0 up to 256).
 hipError_t launch_attn_fwd_generic(const AttnArgs& a);
+// The short-sequence kernel (all keys resident in LDS): Lk <= 128, 32 <= D <= 160.
+bool attn_fwd_short_supported(int D, int Lk);
+hipError_t launch_attn_fwd_short(const AttnArgs& a);
 
 struct SoftmaxArgs {
     const void* a;

@@ -1,21 +1,23 @@
 // attn_fwd.hip -- single-pass attention forward (Eq. 3) for gfx950, with the
 // K and V tiles streamed into LDS by direct global->LDS copies.
 //
-// One workgroup = 4 waves = 128 query rows of one (batch, head); each wave
-// owns 32 rows.  Keys and values move through LDS in tiles of 64 keys; while
-// tiles are consumed, later ones are copied straight from global memory into
-// free buffers (global_load_lds, 16 bytes per lane, no
-// registers involved).  Both tiles keep the row-major [key][d] layout of
-// global memory; a ring of four buffers lets the copy run two tiles ahead.
-// Per tile and wave:
+// One workgroup = 8 waves for 128 query rows of one (batch, head).  Waves
+// 0-3 take the first half of the key tiles and waves 4-7 the second half,
+// each wave owning 32 query rows; at the end the two halves of every row are
+// merged through LDS.  The key split gives four waves per SIMD (each at most
+// 128 VGPRs), which is what hides the latencies of the chain below.
+// Key/value tiles of 64 keys move through LDS double-buffered per half: while
+// one tile is consumed the next is copied straight from global memory
+// (global_load_lds, 16 bytes per lane, no registers involved), keeping the
+// row-major [key][d] layout.  Per 32-key sub-tile and wave:
 //
 //   S^T = K Q^T      32x32x16 MFMA.  A = K rows read from LDS (16 bytes per
 //                    lane), B = Q^T held in registers for the whole kernel.
-//                    The accumulator puts one query per lane (lane % 32) and 16
-//                    of a sub-tile's 32 keys in that lane, so the row maximum
-//                    needs a single exchange between lane halves.
+//                    The accumulator puts one query per lane (lane % 32) and
+//                    16 of the 32 keys in that lane, so the row maximum needs a
+//                    single exchange between lane halves.
 //   p = 2^(c s - m)  c = |scale| log2(e); the running maximum m moves (with
-//                    the matching rescale of O and l) only when a tile's
+//                    the matching rescale of O and l) only when a sub-tile's
 //                    maximum exceeds it by more than 8, so p <= 256.
 //   O^T += V^T P^T   32x32x16 MFMA.  B = P straight from the S^T registers;
 //                    A = V^T, produced from the row-major V tile by the
@@ -28,10 +30,11 @@
 //                    product also yields l in row D of O^T.  Otherwise the
 //                    packed p pairs are summed with v_dot2 against (1, 1).
 //
-// This is the block-wise ("multi-stage") reduction of Sec. 3.2.1 -- a tile's
-// maximum and exponential sum merged into the running pair -- fused with the
-// element-wise normalisation and the product with V, so the N x M matrix A
-// never leaves the chip (the IO-aware tiling of FlashAttention, Sec. 3.2.2).
+// This is the block-wise ("multi-stage") reduction of Sec. 3.2.1 -- a block's
+// maximum and exponential sum merged into the running pair, and the two key
+// halves merged by the same rule -- fused with the element-wise normalisation
+// and the product with V, so the N x M matrix A never leaves the chip (the
+// IO-aware tiling of FlashAttention, Sec. 3.2.2).
 #include "device.h"
 #include "launch.h"
 
@@ -39,10 +42,11 @@ namespace sdattn {
 
 namespace {
 
-constexpr int kWaves = 4;
+constexpr int kQW = 4;                 // query waves, 32 rows each
+constexpr int kWaves = 2 * kQW;        // times two key halves
 constexpr int kThreads = kWaves * 64;
-constexpr int kBQ = kWaves * 32;   // query rows per workgroup
-constexpr int kKB = 64;            // keys per LDS tile
+constexpr int kBQ = kQW * 32;          // query rows per workgroup
+constexpr int kKB = 64;                // keys per LDS tile
 constexpr float kRescaleSlack = 8.0f;
 constexpr int kMaxLds = 160 * 1024;
 
@@ -58,8 +62,13 @@ struct Geom {
     static constexpr int kTileBytes = kKB * D * 2;            // one K or V tile
     static constexpr int kChunks = kTileBytes / 1024;         // 1 KiB wave copies per tile
     static constexpr int kBufBytes = kTileBytes * (kOnes ? 3 : 2);   // K, V (, constant block)
-    static constexpr int kLdsBytes = 4 * kBufBytes;   // a ring of four tile buffers
+    static constexpr int kHalfBytes = 2 * kBufBytes;          // two buffers per key half
+    static constexpr int kMergeFloats = DN * 16 * 64 + 3 * 64;   // one wave's O^T, m, max, l
+    static constexpr int kMergeBytes = kQW * kMergeFloats * 4;
+    static constexpr int kLdsBytes = 2 * kHalfBytes > kMergeBytes ? 2 * kHalfBytes : kMergeBytes;
     static constexpr bool kFits = D >= 32 && D % 8 == 0 && kLdsBytes <= kMaxLds;
+    // waves per SIMD the register budget is sized for (4: 128 VGPRs each)
+    static constexpr int kWavesPerSimd = D <= 64 ? 4 : 2;
 };
 
 // Logical tile for workgroup `bid`.  Workgroups are dealt round-robin over the
@@ -77,7 +86,7 @@ __device__ __forceinline__ u32x2 lds_read_tr(const char* p) {
 }
 
 template <int ET, int D>
-__global__ __launch_bounds__(kThreads) void attn_fwd_lds_kernel(
+__global__ __launch_bounds__(kThreads, Geom<D>::kWavesPerSimd) void attn_fwd_lds_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     uint16_t* __restrict__ O, float* __restrict__ LS, int Lq, int Lk, float scale_abs, float c,
     int neg, int nqb) {
@@ -93,61 +102,58 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_lds_kernel(
     const int l32 = lane & 31;
     const int half = lane >> 5;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int kh = wave / kQW;         // key half of this wave
+    const int wq = wave % kQW;         // query slot of this wave
 
     const int tile = xcd_remap(blockIdx.x, gridDim.x);
     const int bh = tile / nqb;
     const int qb = tile - bh * nqb;
-    const int q0 = qb * kBQ + wave * 32;
+    const int q0 = qb * kBQ + wq * 32;
 
     const char* Kh = (const char*)(K + (size_t)bh * Lk * D);
     const char* Vh = (const char*)(V + (size_t)bh * Lk * D);
+    char* hbase = smem + kh * G::kHalfBytes;   // this half's two buffers
 
     // Constant blocks (one per buffer): a one in column 0 of every row, zeros
     // elsewhere.  Lanes whose d lies at or past D read these instead of V.
     if constexpr (G::kOnes) {
-#pragma unroll
-        for (int b = 0; b < 4; ++b) {
-            uint16_t* cb = (uint16_t*)(smem + b * G::kBufBytes + 2 * TB);
-            for (int i = tid; i < kKB * D; i += kThreads)
-                cb[i] = (i % D == 0) ? from_float<ET>(1.0f) : (uint16_t)0;
+        const uint32_t one = from_float<ET>(1.0f);
+        for (int i = tid; i < 4 * (TB / 16); i += kThreads) {
+            const int b = i / (TB / 16), j = i - b * (TB / 16);
+            u32x4 w = {0u, 0u, 0u, 0u};
+            if ((j * 8) % D == 0) w[0] = one;
+            *(u32x4*)(smem + b * G::kBufBytes + 2 * TB + j * 16) = w;
         }
     }
 
-    // Copy key tile [kbase, kbase + 64) of K and V into buffer b.  Wave w
-    // issues the 1 KiB pieces w, w + 4, ...; in a tail tile (TAIL), rows past
-    // Lk repeat row Lk - 1 (finite data; their weights are forced to zero).
-    auto issue_tile = [&](auto tail_c, int kbase, int b) __attribute__((always_inline)) {
-        constexpr bool TAIL = decltype(tail_c)::value;
+    // Tiles of this half: [t_first, t_first + t_count).  Half 0 takes the
+    // first ceil(ntiles / 2), half 1 the rest; both run nh steps.
+    const int ntiles = (Lk + kKB - 1) / kKB;
+    const int nh = (ntiles + 1) / 2;
+    const int t_first = kh ? nh : 0;
+    const int t_count = kh ? ntiles - nh : nh;
+
+    // Copy tile t of this half into its buffer b (the half's 4 waves issue
+    // the 1 KiB pieces wq, wq + 4, ...).  Rows past Lk repeat row Lk - 1
+    // (finite data; their weights are forced to zero).
+    auto issue_tile = [&](int t, int b) __attribute__((always_inline)) {
+        const int kbase = t * kKB;
+        const bool tail = kbase + kKB > Lk;
 #pragma unroll
-        for (int i = 0; i < (2 * G::kChunks + kWaves - 1) / kWaves; ++i) {
-            const int cidx = wave + kWaves * i;
+        for (int i = 0; i < (2 * G::kChunks + kQW - 1) / kQW; ++i) {
+            const int cidx = wq + kQW * i;
             if (cidx < 2 * G::kChunks) {
                 const bool isv = cidx >= G::kChunks;
                 const int cc = isv ? cidx - G::kChunks : cidx;
-                const char* src = isv ? Vh : Kh;
                 const int byte = cc * 1024 + lane * 16;
-                size_t goff;
-                if constexpr (TAIL) {
-                    const int row = byte / (2 * D);
-                    const int col = byte - row * (2 * D);
-                    const int grow = min(kbase + row, Lk - 1);
-                    goff = (size_t)grow * (2 * D) + col;
-                } else {
-                    goff = (size_t)kbase * (2 * D) + byte;
-                }
-                char* dst = smem + b * G::kBufBytes + (isv ? TB : 0) + cc * 1024;
-                __builtin_amdgcn_global_load_lds(src + goff, (lds_void_t*)dst, 16, 0, 0);
+                const int row = byte / (2 * D);
+                const int col = byte - row * (2 * D);
+                const int grow = tail ? min(kbase + row, Lk - 1) : kbase + row;
+                const size_t goff = (size_t)grow * (2 * D) + col;
+                char* dst = hbase + b * G::kBufBytes + (isv ? TB : 0) + cc * 1024;
+                __builtin_amdgcn_global_load_lds((isv ? Vh : Kh) + goff, (lds_void_t*)dst, 16, 0, 0);
             }
         }
-    };
-    std::integral_constant<bool, false> full_c;
-    std::integral_constant<bool, true> tail_c;
-    const int nfull = Lk / kKB;
-    const int ntiles = (Lk + kKB - 1) / kKB;
-    // copy tile t (full or tail) into buffer t % 4, if it exists
-    auto issue = [&](int t) __attribute__((always_inline)) {
-        if (t < nfull) issue_tile(full_c, t * kKB, t & 3);
-        else if (t < ntiles) issue_tile(tail_c, t * kKB, t & 3);
     };
 
     // Q^T operand: lane holds query q0 + l32, d = 16s + 8*half .. +7 for each s.
@@ -163,7 +169,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_lds_kernel(
     }
 
     // Per-lane LDS byte offsets inside a buffer.
-    // K rows: lane reads key row l32 at d = 8*half (+16 s, +32 t rows).
+    // K rows: lane reads key row l32 at d = 8*half (+16 s, +32 sub rows).
     const int k_off = (l32 * D + 8 * half) * 2;
     // V^T via transposing reads: 16-lane group g = lane / 16 covers keys
     // 4*(g/2) .. +3 and d = 32n + 16*(g%2) .. +15; its lane i points at key
@@ -188,209 +194,132 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_lds_kernel(
     float s_max = -__builtin_inff();   // true running max of the raw scores
     float l_part = 0.0f;               // this lane's part of the row sum (v_dot2 path)
 
-    struct Scores { f32x16 v[2]; };    // S^T of a tile's two 32-key sub-tiles
-    struct Probs { u32x4 v[2][2]; };   // its rounded p as four P^T operands
-
-    // S^T = K Q^T for the tile in buffer BUF
-    auto qk = [&](auto buf_c) __attribute__((always_inline)) {
-        constexpr int BUF = decltype(buf_c)::value;
-        const char* base = smem + BUF * G::kBufBytes;
-        Scores st;
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {
-#pragma unroll
-            for (int r = 0; r < 16; ++r) st.v[t][r] = 0.0f;
-#pragma unroll
-            for (int s = 0; s < DK; ++s) {
-                const u32x4 a = *(const u32x4*)(base + k_off + (32 * t * D + 16 * s) * 2);
-                st.v[t] = mfma32x32x16<ET>(a, qreg[s], st.v[t]);
-            }
-        }
-        return st;
-    };
-
-    // O^T += V^T P^T with V from buffer BUF; keys of operand slot e are
-    // 32t + 16u + 8*(e/4) + 4*half + e%4
-    auto pv = [&](auto buf_c, const Probs& pk) __attribute__((always_inline)) {
-        constexpr int BUF = decltype(buf_c)::value;
-        const char* base = smem + BUF * G::kBufBytes;
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-#pragma unroll
-            for (int u = 0; u < 2; ++u)
-#pragma unroll
-                for (int n = 0; n < DN; ++n) {
-                    const char* vb = base + v_off[n];
-                    const u32x2 lo = lds_read_tr(vb + (32 * t + 16 * u) * D * 2);
-                    const u32x2 hi = lds_read_tr(vb + (32 * t + 16 * u + 8) * D * 2);
-                    const u32x4 a = {lo[0], lo[1], hi[0], hi[1]};
-                    acc[n] = mfma32x32x16<ET>(a, pk.v[t][u], acc[n]);
-                }
-    };
-
-    // Softmax step of a tile (keys kbase ..): merge its row maximum into the
-    // running one, p = 2^(c s - m) rounded to the input type.  The decision
-    // to move m is wave-uniform and taken without a branch; the matching
-    // rescale of O (alpha != 1) is left to the caller, after the MFMAs that
-    // still accumulate the previous tile into O.
-    auto softmax = [&](auto tail_c, Scores st, int kbase, float& alpha, bool& moved)
-                       __attribute__((always_inline)) {
+    // One 32-key sub-tile (keys kbase ..) held at row offset `sub` * 32 of
+    // the tile in buffer base `buf`.
+    auto step32 = [&](auto tail_c, const char* buf, int sub, int kbase) __attribute__((always_inline)) {
         constexpr bool TAIL = decltype(tail_c)::value;
+        // ---- S^T = K Q^T
+        f32x16 st;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) st[r] = 0.0f;
+#pragma unroll
+        for (int s = 0; s < DK; ++s) {
+            const u32x4 a = *(const u32x4*)(buf + k_off + (32 * sub * D + 16 * s) * 2);
+            st = mfma32x32x16<ET>(a, qreg[s], st);
+        }
         if constexpr (TAIL) {
 #pragma unroll
-            for (int t = 0; t < 2; ++t)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int key = kbase + 32 * t + 8 * (r >> 2) + 4 * half + (r & 3);
-                    if (key >= Lk) st.v[t][r] = -__builtin_inff();
-                }
+            for (int r = 0; r < 16; ++r) {
+                const int key = kbase + 8 * (r >> 2) + 4 * half + (r & 3);
+                if (key >= Lk) st[r] = -__builtin_inff();
+            }
         }
-        float mloc = st.v[0][0];
+        // ---- row maximum merged into the running one
+        float mloc = st[0];
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, st.v[t][r]);
+        for (int r = 1; r < 16; ++r) mloc = fmaxf(mloc, st[r]);
         mloc = half_max(mloc);
         s_max = fmaxf(s_max, mloc);
         const float mb = mloc * c;
-        moved = __any(mb > m_run + kRescaleSlack);
-        const float m_new = moved ? fmaxf(m_run, mb) : m_run;
-        alpha = moved ? fast_exp2(m_run - m_new) : 1.0f;
-        m_run = m_new;
+        if (__any(mb > m_run + kRescaleSlack)) {
+            const float m_new = fmaxf(m_run, mb);
+            const float alpha = fast_exp2(m_run - m_new);
+#pragma unroll
+            for (int n = 0; n < DN; ++n)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[n][r] *= alpha;
+            l_part *= alpha;
+            m_run = m_new;
+        }
+        // ---- p = 2^(c s - m), rounded to the input type
         const float negm = -m_run;
-        Probs pk;
-        if constexpr (!G::kOnes) l_part *= alpha;
+        float p[16];
 #pragma unroll
-        for (int t = 0; t < 2; ++t) {
-            float p[16];
+        for (int r = 0; r < 16; ++r) p[r] = fast_exp2(fmaf(st[r], c, negm));
+        if constexpr (TAIL) {
 #pragma unroll
-            for (int r = 0; r < 16; ++r) p[r] = fast_exp2(fmaf(st.v[t][r], c, negm));
-            if constexpr (TAIL) {
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int key = kbase + 32 * t + 8 * (r >> 2) + 4 * half + (r & 3);
-                    if (key >= Lk) p[r] = 0.0f;
-                }
+            for (int r = 0; r < 16; ++r) {
+                const int key = kbase + 8 * (r >> 2) + 4 * half + (r & 3);
+                if (key >= Lk) p[r] = 0.0f;
             }
+        }
+        u32x4 pk[2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+            for (int w = 0; w < 4; ++w) pk[u][w] = pack2<ET>(p[8 * u + 2 * w], p[8 * u + 2 * w + 1]);
+        if constexpr (!G::kOnes) {
 #pragma unroll
             for (int u = 0; u < 2; ++u)
 #pragma unroll
-                for (int w = 0; w < 4; ++w) pk.v[t][u][w] = pack2<ET>(p[8 * u + 2 * w], p[8 * u + 2 * w + 1]);
-            if constexpr (!G::kOnes) {
-#pragma unroll
-                for (int u = 0; u < 2; ++u)
-#pragma unroll
-                    for (int w = 0; w < 4; ++w) l_part = add_pair<ET>(pk.v[t][u][w], l_part);
-            }
+                for (int w = 0; w < 4; ++w) l_part = add_pair<ET>(pk[u][w], l_part);
         }
-        return pk;
+        // ---- O^T += V^T P^T; keys of operand slot e: 16u + 8*(e/4) + 4*half + e%4
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+            for (int n = 0; n < DN; ++n) {
+                const char* vb = buf + v_off[n] + (32 * sub + 16 * u) * D * 2;
+                const u32x2 lo = lds_read_tr(vb);
+                const u32x2 hi = lds_read_tr(vb + 8 * D * 2);
+                const u32x4 a = {lo[0], lo[1], hi[0], hi[1]};
+                acc[n] = mfma32x32x16<ET>(a, pk[u], acc[n]);
+            }
     };
 
-    auto rescale = [&](float alpha) __attribute__((always_inline)) {
+    std::integral_constant<bool, false> full_c;
+    std::integral_constant<bool, true> tail_c;
+
+    // consume the tile t (in buffer b) of this half
+    auto consume = [&](int t, int b) __attribute__((always_inline)) {
+        const char* buf = hbase + b * G::kBufBytes;
+        const int kbase = t * kKB;
+        if (kbase + kKB <= Lk) {
+            step32(full_c, buf, 0, kbase);
+            step32(full_c, buf, 1, kbase + 32);
+        } else {
+            if (kbase + 32 <= Lk) step32(full_c, buf, 0, kbase);
+            else step32(tail_c, buf, 0, kbase);
+            if (kbase + 32 < Lk) step32(tail_c, buf, 1, kbase + 32);
+        }
+    };
+
+    if (t_count > 0) issue_tile(t_first, 0);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    for (int i = 0; i < nh; ++i) {
+        const int b = i & 1;
+        if (i + 1 < t_count) issue_tile(t_first + i + 1, b ^ 1);
+        if (i < t_count) consume(t_first + i, b);
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+    }
+
+    // ---- merge the two key halves of every row (the block-merge rule)
+    float* mrg = (float*)smem + wq * G::kMergeFloats;
+    if (kh == 1) {
 #pragma unroll
         for (int n = 0; n < DN; ++n)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) acc[n][r] *= alpha;
-    };
-
-    // Interleave the step's matrix-core work (P V of the previous tile, then
-    // S of the next) with the softmax of the current tile: one MFMA, a few
-    // LDS reads for the next MFMA, then a run of vector instructions.
-    auto interleave = [&]() __attribute__((always_inline)) {
-        constexpr int kPV = 4 * DN, kQK = 2 * DK;
-        __builtin_amdgcn_sched_group_barrier(0x100, 2 * kPV + kQK, 0);   // every LDS read first
-#pragma unroll
-        for (int i = 0; i < kPV; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
-            __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);   // VALU
-        }
-#pragma unroll
-        for (int i = 0; i < kQK; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
-        }
-    };
-
-    // Software pipeline over tiles, four LDS buffers (tile t lives in buffer
-    // t % 4).  A middle step j (tile j full, tile j+1 present):
-    //   - starts copying tile j+2,
-    //   - multiplies the previous tile's P by V (tile j-1),
-    //   - does the softmax of tile j (its scores are already in registers),
-    //   - computes the scores of tile j+1,
-    // so the matrix cores work on tiles j-1 and j+1 while the vector ALU works
-    // on tile j.  One barrier per step publishes tile j+2 and frees buffer
-    // (j-1) % 4 for the copy issued at step j+1.
-    Scores S;      // scores of the tile being softmaxed
-    Probs P;       // probabilities of the tile before it
-
-    auto mid_step = [&](auto bj_c, auto has_prev_c, int j) __attribute__((always_inline)) {
-        constexpr int BJ = decltype(bj_c)::value;   // j % 4
-        constexpr bool PREV = decltype(has_prev_c)::value;
-        std::integral_constant<int, (BJ + 1) % 4> bn_c;
-        std::integral_constant<int, (BJ + 3) % 4> bp_c;
-        issue(j + 2);
-        if constexpr (PREV) pv(bp_c, P);
-        float alpha;
-        bool moved;
-        const Probs pc = softmax(full_c, S, j * kKB, alpha, moved);
-        S = qk(bn_c);
-        interleave();
-        if (moved) rescale(alpha);
-        P = pc;
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
-    };
-
-    // The last tile (j = ntiles - 1): previous P V, masked softmax, own P V.
-    auto last_step = [&](auto bj_c, auto has_prev_c, int j) __attribute__((always_inline)) {
-        constexpr int BJ = decltype(bj_c)::value;
-        constexpr bool PREV = decltype(has_prev_c)::value;
-        std::integral_constant<int, (BJ + 3) % 4> bp_c;
-        if constexpr (PREV) pv(bp_c, P);
-        float alpha;
-        bool moved;
-        const Probs pc = (j < nfull) ? softmax(full_c, S, j * kKB, alpha, moved)
-                                     : softmax(tail_c, S, j * kKB, alpha, moved);
-        if (moved) rescale(alpha);
-        pv(bj_c, pc);
-    };
-
-    std::integral_constant<int, 0> c0;
-    std::integral_constant<int, 1> c1;
-    std::integral_constant<int, 2> c2;
-    std::integral_constant<int, 3> c3;
-    std::integral_constant<bool, false> noprev_c;
-    std::integral_constant<bool, true> prev_c;
-
-    issue(0);
-    issue(1);
-    __builtin_amdgcn_s_waitcnt(0);
+            for (int r = 0; r < 16; ++r) mrg[(n * 16 + r) * 64 + lane] = acc[n][r];
+        mrg[DN * 16 * 64 + lane] = m_run;
+        mrg[DN * 16 * 64 + 64 + lane] = s_max;
+        mrg[DN * 16 * 64 + 128 + lane] = l_part;
+    }
     __syncthreads();
-    S = qk(c0);
-    if (ntiles == 1) {
-        last_step(c0, noprev_c, 0);
-    } else {
-        mid_step(c0, noprev_c, 0);
-        int j = 1;
-        for (; j + 4 < ntiles; j += 4) {
-            mid_step(c1, prev_c, j);
-            mid_step(c2, prev_c, j + 1);
-            mid_step(c3, prev_c, j + 2);
-            mid_step(c0, prev_c, j + 3);
-        }
-        if (j + 1 < ntiles) {
-            mid_step(c1, prev_c, j++);
-            if (j + 1 < ntiles) {
-                mid_step(c2, prev_c, j++);
-                if (j + 1 < ntiles) mid_step(c3, prev_c, j++);
-            }
-        }
-        switch (j & 3) {
-            case 0: last_step(c0, prev_c, j); break;
-            case 1: last_step(c1, prev_c, j); break;
-            case 2: last_step(c2, prev_c, j); break;
-            default: last_step(c3, prev_c, j); break;
-        }
+    if (kh == 1) return;
+    {
+        const float m_b = mrg[DN * 16 * 64 + lane];
+        const float m_new = fmaxf(m_run, m_b);
+        const float a0 = fast_exp2(m_run - m_new);   // exp2(-inf) = 0 for an empty half
+        const float a1 = fast_exp2(m_b - m_new);
+#pragma unroll
+        for (int n = 0; n < DN; ++n)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[n][r] = acc[n][r] * a0 + mrg[(n * 16 + r) * 64 + lane] * a1;
+        s_max = fmaxf(s_max, mrg[DN * 16 * 64 + 64 + lane]);
+        l_part = l_part * a0 + mrg[DN * 16 * 64 + 128 + lane] * a1;
+        m_run = m_new;
     }
 
     // ---- epilogue: l, O / l, store

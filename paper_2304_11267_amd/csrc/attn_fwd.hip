@@ -85,7 +85,7 @@ __device__ __forceinline__ u32x2 lds_read_tr(const char* p) {
     return __builtin_bit_cast(u32x2, v);
 }
 
-template <int ET, int D>
+template <int ET, int D, bool STATS>
 __global__ __launch_bounds__(kThreads, Geom<D>::kWavesPerSimd) void attn_fwd_lds_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     uint16_t* __restrict__ O, float* __restrict__ LS, int Lq, int Lk, float scale_abs, float c,
@@ -194,9 +194,20 @@ __global__ __launch_bounds__(kThreads, Geom<D>::kWavesPerSimd) void attn_fwd_lds
     float s_max = -__builtin_inff();   // true running max of the raw scores
     float l_part = 0.0f;               // this lane's part of the row sum (v_dot2 path)
 
+    // How a sub-tile treats the running maximum m (log2 units):
+    //   kFirst  the wave's first sub-tile: m = its row maximum (O is still 0)
+    //   kFixed  m stays; p = 2^(c s - m) may exceed 1, and if a later logit
+    //           exceeds m by more than ~16 the rounded p overflows to inf,
+    //           which the overflow vote after the loop detects
+    //   kOnline m moves (with the rescale of O and l) whenever a sub-tile's
+    //           maximum exceeds it by more than 8 -- the fallback
+    enum { kFirst = 0, kFixed = 1, kOnline = 2 };
+
     // One 32-key sub-tile (keys kbase ..) held at row offset `sub` * 32 of
     // the tile in buffer base `buf`.
-    auto step32 = [&](auto tail_c, const char* buf, int sub, int kbase) __attribute__((always_inline)) {
+    auto step32 = [&](auto mode_c, auto tail_c, const char* buf, int sub, int kbase)
+                      __attribute__((always_inline)) {
+        constexpr int MODE = decltype(mode_c)::value;
         constexpr bool TAIL = decltype(tail_c)::value;
         // ---- S^T = K Q^T
         f32x16 st;
@@ -214,22 +225,28 @@ __global__ __launch_bounds__(kThreads, Geom<D>::kWavesPerSimd) void attn_fwd_lds
                 if (key >= Lk) st[r] = -__builtin_inff();
             }
         }
-        // ---- row maximum merged into the running one
-        float mloc = st[0];
+        // ---- row maximum (Eq. 4's L), where the mode needs it
+        if constexpr (MODE != kFixed || STATS) {
+            float mloc = st[0];
 #pragma unroll
-        for (int r = 1; r < 16; ++r) mloc = fmaxf(mloc, st[r]);
-        mloc = half_max(mloc);
-        s_max = fmaxf(s_max, mloc);
-        const float mb = mloc * c;
-        if (__any(mb > m_run + kRescaleSlack)) {
-            const float m_new = fmaxf(m_run, mb);
-            const float alpha = fast_exp2(m_run - m_new);
+            for (int r = 1; r < 16; ++r) mloc = fmaxf(mloc, st[r]);
+            mloc = half_max(mloc);
+            s_max = fmaxf(s_max, mloc);
+            if constexpr (MODE == kFirst) {
+                m_run = mloc * c;
+            } else if constexpr (MODE == kOnline) {
+                const float mb = mloc * c;
+                if (__any(mb > m_run + kRescaleSlack)) {
+                    const float m_new = fmaxf(m_run, mb);
+                    const float alpha = fast_exp2(m_run - m_new);
 #pragma unroll
-            for (int n = 0; n < DN; ++n)
+                    for (int n = 0; n < DN; ++n)
 #pragma unroll
-                for (int r = 0; r < 16; ++r) acc[n][r] *= alpha;
-            l_part *= alpha;
-            m_run = m_new;
+                        for (int r = 0; r < 16; ++r) acc[n][r] *= alpha;
+                    l_part *= alpha;
+                    m_run = m_new;
+                }
+            }
         }
         // ---- p = 2^(c s - m), rounded to the input type
         const float negm = -m_run;
@@ -269,30 +286,80 @@ __global__ __launch_bounds__(kThreads, Geom<D>::kWavesPerSimd) void attn_fwd_lds
 
     std::integral_constant<bool, false> full_c;
     std::integral_constant<bool, true> tail_c;
+    std::integral_constant<int, kFirst> first_c;
+    std::integral_constant<int, kFixed> fixed_c;
+    std::integral_constant<int, kOnline> online_c;
 
-    // consume the tile t (in buffer b) of this half
-    auto consume = [&](int t, int b) __attribute__((always_inline)) {
+    // consume the tile t (in buffer b) of this half; its first sub-tile in
+    // mode mode0_c, the second in mode_c
+    auto consume = [&](auto mode0_c, auto mode_c, int t, int b) __attribute__((always_inline)) {
         const char* buf = hbase + b * G::kBufBytes;
         const int kbase = t * kKB;
         if (kbase + kKB <= Lk) {
-            step32(full_c, buf, 0, kbase);
-            step32(full_c, buf, 1, kbase + 32);
+            step32(mode0_c, full_c, buf, 0, kbase);
+            step32(mode_c, full_c, buf, 1, kbase + 32);
         } else {
-            if (kbase + 32 <= Lk) step32(full_c, buf, 0, kbase);
-            else step32(tail_c, buf, 0, kbase);
-            if (kbase + 32 < Lk) step32(tail_c, buf, 1, kbase + 32);
+            if (kbase + 32 <= Lk) step32(mode0_c, full_c, buf, 0, kbase);
+            else step32(mode0_c, tail_c, buf, 0, kbase);
+            if (kbase + 32 < Lk) step32(mode_c, tail_c, buf, 1, kbase + 32);
         }
     };
 
-    if (t_count > 0) issue_tile(t_first, 0);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    for (int i = 0; i < nh; ++i) {
-        const int b = i & 1;
-        if (i + 1 < t_count) issue_tile(t_first + i + 1, b ^ 1);
-        if (i < t_count) consume(t_first + i, b);
+    // all tiles of this half: the first tile opens with kFirst, every other
+    // sub-tile runs in mode_c (kFixed, or kOnline for the fallback)
+    auto run_tiles = [&](auto mode_c) __attribute__((always_inline)) {
+        if (t_count > 0) issue_tile(t_first, 0);
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
+        if (t_count > 0) {
+            if (t_count > 1) issue_tile(t_first + 1, 1);
+            consume(first_c, mode_c, t_first, 0);
+        }
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        for (int i = 1; i < nh; ++i) {
+            const int b = i & 1;
+            if (i + 1 < t_count) issue_tile(t_first + i + 1, b ^ 1);
+            if (i < t_count) consume(mode_c, mode_c, t_first + i, b);
+            __builtin_amdgcn_s_waitcnt(0);
+            __syncthreads();
+        }
+    };
+
+    run_tiles(fixed_c);
+    // Overflow vote: with m fixed at the first sub-tile's maximum, a later
+    // logit larger by more than ~16 (log2) overflows the rounded p to inf,
+    // which makes this lane's row sum non-finite.  Any such row sends the
+    // whole workgroup (it shares the LDS tiles) through the online path.
+    {
+        float l_check;
+        if constexpr (G::kOnes) {
+            constexpr int dd = D % 32;
+            constexpr int rsel = 4 * (dd >> 3) + (dd & 3);
+            l_check = acc[D / 32][rsel];
+        } else {
+            l_check = l_part;
+        }
+        const bool overflow = !(__builtin_fabsf(l_check) < __builtin_inff());
+        // workgroup-wide OR through the (now idle) first LDS words
+        int* vote = (int*)smem;
+        const int wave_overflow = __any(overflow) ? 1 : 0;   // ballot with every lane active
+        if (lane == 0) vote[wave] = wave_overflow;
+        __syncthreads();
+        int any = 0;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) any |= vote[w];
+        __syncthreads();
+        if (any) {
+#pragma unroll
+            for (int n = 0; n < DN; ++n)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[n][r] = 0.0f;
+            m_run = -__builtin_inff();
+            s_max = -__builtin_inff();
+            l_part = 0.0f;
+            run_tiles(online_c);
+        }
     }
 
     // ---- merge the two key halves of every row (the block-merge rule)
@@ -367,11 +434,16 @@ hipError_t launch_d(const AttnArgs& a) {
         const long long nblk = (long long)a.B * a.H * nqb;
         const float scale_abs = a.scale < 0 ? -a.scale : a.scale;
         const float c = scale_abs * kLog2e;
-        static const hipError_t attr = hipFuncSetAttribute(
-            reinterpret_cast<const void*>(&attn_fwd_lds_kernel<ET, D>),
+        static const hipError_t attr0 = hipFuncSetAttribute(
+            reinterpret_cast<const void*>(&attn_fwd_lds_kernel<ET, D, false>),
             hipFuncAttributeMaxDynamicSharedMemorySize, G::kLdsBytes);
-        if (attr != hipSuccess) return attr;
-        hipLaunchKernelGGL((attn_fwd_lds_kernel<ET, D>), dim3((unsigned)nblk), dim3(kThreads),
+        static const hipError_t attr1 = hipFuncSetAttribute(
+            reinterpret_cast<const void*>(&attn_fwd_lds_kernel<ET, D, true>),
+            hipFuncAttributeMaxDynamicSharedMemorySize, G::kLdsBytes);
+        if (attr0 != hipSuccess) return attr0;
+        if (attr1 != hipSuccess) return attr1;
+        auto kern = a.ls ? attn_fwd_lds_kernel<ET, D, true> : attn_fwd_lds_kernel<ET, D, false>;
+        hipLaunchKernelGGL(kern, dim3((unsigned)nblk), dim3(kThreads),
                            G::kLdsBytes, (hipStream_t)a.stream, (const uint16_t*)a.q,
                            (const uint16_t*)a.k, (const uint16_t*)a.v, (uint16_t*)a.out, a.ls,
                            a.Lq, a.Lk, scale_abs, c, a.scale < 0 ? 1 : 0, nqb);

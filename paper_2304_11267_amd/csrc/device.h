@@ -86,6 +86,13 @@ __device__ __forceinline__ float add_pair(uint32_t w, float acc) {
     }
 }
 
+// s_waitcnt immediate that waits until at most n vector-memory loads are
+// outstanding (gfx9 encoding: vmcnt in bits 3:0 and 15:14; expcnt and
+// lgkmcnt left at their maxima, i.e. not waited on).
+constexpr int vm_wait(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+// s_waitcnt immediate that waits for every LDS operation (lgkmcnt = 0) only.
+constexpr int lgkm_wait0() { return 15 | (3 << 14) | (7 << 4); }
+
 // 2^x on the transcendental unit (v_exp_f32); exp2(-inf) = 0.
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 

@@ -242,3 +242,36 @@ def test_softmax_rows_on_attention_logits_matches_forward_stats():
     ls_fwd = ls_fwd.reshape(-1, 2)
     assert np.max(np.abs(ls_rows[:, 0] - ls_fwd[:, 0])) <= 1e-5 * np.abs(ls_rows[:, 0]).max()
     assert np.max(np.abs(ls_rows[:, 1] - ls_fwd[:, 1]) / ls_rows[:, 1]) <= 2e-3
+
+
+# ------------------------------------ the fixed-maximum path and its fallback
+
+@pytest.mark.parametrize("Lk,D", [(300, 40), (1024, 80), (4096, 40), (520, 64)])
+def test_late_dominant_keys_overflow_fast_path_and_fall_back(Lk, D):
+    """Keys far larger than the first 32 of each key half: with the reference
+    maximum fixed at the first sub-tile, p overflows, and the kernel must fall
+    back to the running-maximum path and still match the oracle."""
+    rng = np.random.default_rng(Lk + D)
+    B, H, Lq = 1, 2, 160
+    q = np.zeros((B, H, Lq, D), np.float16)
+    q[..., 0] = 8.0
+    q[..., 1:] = (rng.standard_normal((B, H, Lq, D - 1)) * 0.1).astype(np.float16)
+    k = (rng.standard_normal((B, H, Lk, D)) * 0.1).astype(np.float16)
+    v = rng.standard_normal((B, H, Lk, D)).astype(np.float16)
+    ntiles = (Lk + 63) // 64
+    nh = (ntiles + 1) // 2
+    for j in (40, 77, nh * 64 + 40, Lk - 1):      # past the first sub-tile of each half
+        if j < Lk:
+            k[..., j, 0] = 8.0                    # logit 64 vs ~0 elsewhere (scale 1)
+    check_case(q, k, v, 1.0, what=f"late dominant keys Lk={Lk} D={D}")
+
+
+@pytest.mark.parametrize("Lk,D", [(2048, 40), (700, 80)])
+def test_key_norms_growing_along_the_sequence(Lk, D):
+    rng = np.random.default_rng(7 * Lk + D)
+    q = rng.standard_normal((2, 2, 256, D)).astype(np.float16)
+    grow = (1.0 + 3.0 * np.arange(Lk) / Lk)[None, None, :, None]
+    k = (rng.standard_normal((2, 2, Lk, D)) * grow).astype(np.float16)
+    v = rng.standard_normal((2, 2, Lk, D)).astype(np.float16)
+    for scale in (float(np.float32(1 / np.sqrt(D))), 1.0):
+        check_case(q, k, v, scale, what=f"growing norms Lk={Lk} D={D} scale={scale}")

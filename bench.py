@@ -115,7 +115,7 @@ def main():
         "peak": PEAK_F16_TFLOPS,
         "unit": "TFLOP/s",
         "frac": round(self_tflops / PEAK_F16_TFLOPS, 4),
-        "traffic": None,
+        "traffic": recorded_traffic(),
         "avg_kernel_us": round(self_ms * 1e3, 3),
         "flops_per_launch": self_case.flops,
     }
@@ -173,6 +173,9 @@ def cold_cross(torch, sd, wl, dev, stream, case, nsets=40, reps=3):
     times = []
     for _ in range(reps):
         evs = [torch.cuda.Event(enable_timing=True) for _ in range(nsets + 1)]
+        # keep the GPU busy while the launches are queued, so the events time
+        # back-to-back kernels rather than the host's launch rate
+        torch.cuda._sleep(20_000_000)
         evs[0].record(stream)
         for i, s in enumerate(sets):
             sd.forward(*s, case.scale, stream)
@@ -227,6 +230,24 @@ def copy_calibration(torch, dev, stream, nbytes=256 << 20, reps=3):
     ms = e0.elapsed_time(e1) / reps
     return {"bytes_read": nbytes, "bytes_written": nbytes, "avg_kernel_us": round(ms * 1e3, 2),
             "gbs": round(2 * nbytes / (ms * 1e-3) / 1e9, 1)}
+
+
+def recorded_traffic():
+    """HBM bytes per launch of the 64x64 self-attention kernel from the
+    committed rocprofv3 counter runs (FETCH_SIZE, WRITE_SIZE, scaled by a plain
+    copy's readings), or None when the kernel source changed since."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "attn_l64_self_hbm_traffic.json")
+    try:
+        rec = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    h = hashlib.sha256()
+    for f in rec["sources"]:
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    if h.hexdigest() != rec["sources_sha256"]:
+        return None
+    return int(rec["fetch_kib"] * rec["fetch_scale"] * 1024 + rec["write_kib"] * rec["write_scale"] * 1024)
 
 
 def cpu_baseline(wl, self_case, cross_case, rows_per_head):

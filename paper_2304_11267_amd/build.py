@@ -32,10 +32,16 @@ CFLAGS = [
     "-mllvm", "-amdgpu-mfma-vgpr-form",
 ]
 
+# Per-file additions.  The short-sequence kernel is latency-bound: its first 14
+# argument dwords arrive preloaded in SGPRs instead of through scalar loads.
+EXTRA_FLAGS = {
+    "attn_fwd_short.hip": ["-mllvm", "-amdgpu-kernarg-preload-count=14"],
+}
+
 
 def _compile(src: str, verbose: bool) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *CFLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *CFLAGS, *EXTRA_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -107,6 +107,37 @@ def test_ragged_shapes(shape):
     check_case(q, k, v, float(np.float32(1 / np.sqrt(D))), what=str(shape))
 
 
+# Short key sequences (the text context, Lk <= 128): every count of 32-key
+# sub-tiles, Lk on, just past and just short of each 16- and 32-key boundary,
+# and Lq = 97 so a workgroup holds one full 32-row strip, one partial strip
+# and two strips wholly past Lq.
+SHORT_LK = [1, 2, 15, 16, 17, 31, 32, 33, 48, 49, 63, 64, 65, 77, 80, 95, 96, 97, 112, 113,
+            127, 128]
+SHORT_D = [32, 40, 56, 80, 96, 160]
+
+
+@pytest.mark.parametrize("D", SHORT_D)
+@pytest.mark.parametrize("Lk", SHORT_LK)
+def test_short_key_sequences(Lk, D):
+    q, k, v = wl.make_qkv(1, 2, 97, Lk, D, 3000 + 7 * Lk + D)
+    check_case(q, k, v, float(np.float32(1 / np.sqrt(D))), what=f"Lk={Lk} D={D}")
+
+
+@pytest.mark.parametrize("Lk,D", [(33, 40), (77, 80), (128, 160), (49, 96)])
+def test_short_key_sequences_bf16(Lk, D):
+    q, k, v = wl.make_qkv(2, 1, 161, Lk, D, 3500 + Lk + D, dtype="bf16")
+    check_case(q, k, v, float(np.float32(1 / np.sqrt(D))), dtype="bf16", what=f"Lk={Lk} D={D}")
+
+
+@pytest.mark.parametrize("Lk,D", [(77, 40), (77, 160), (20, 80)])
+def test_statistics_output_does_not_change_o(Lk, D):
+    q, k, v = wl.make_qkv(2, 2, 300, Lk, D, 3600 + Lk + D)
+    scale = float(np.float32(1 / np.sqrt(D)))
+    o_plain = run_forward(q, k, v, scale)
+    o_stats, _ = run_forward(q, k, v, scale, want_ls=True)
+    assert np.array_equal(o_plain, o_stats)
+
+
 @pytest.mark.parametrize("scale", [0.0, -0.2, 1.0])
 def test_scale_values(scale):
     q, k, v = wl.make_qkv(1, 2, 70, 90, 40, 901)

@@ -100,8 +100,9 @@ __global__ __launch_bounds__(W * 64) void attn_fwd_short_kernel(
     const char* Kh = (const char*)(K + (size_t)bh * Lk * D);
     const char* Vh = (const char*)(V + (size_t)bh * Lk * D);
 
-    // K and V rows 0 .. 32*NS - 1, 1 KiB per wave copy: K rows past Lk repeat
-    // row Lk - 1, V rows past Lk are zero.
+    // K and V rows 0 .. 32*NS - 1, 1 KiB per wave copy of the contiguous rows
+    // below Lk; past them K repeats row Lk - 1 and V is zero.
+    const int kv_bytes = Lk * (2 * D);
 #pragma unroll
     for (int i = 0; i < (2 * G::kChunks + W - 1) / W; ++i) {
         const int cidx = wave + W * i;
@@ -109,15 +110,19 @@ __global__ __launch_bounds__(W * 64) void attn_fwd_short_kernel(
             const bool isv = cidx >= G::kChunks;
             const int cc = isv ? cidx - G::kChunks : cidx;
             const int byte = cc * 1024 + lane * 16;
-            if (byte < BB) {
-                const int row = byte / (2 * D);
-                const int col = byte - row * (2 * D);
-                char* dst = smem + (isv ? G::kV : 0) + cc * 1024;
-                if (isv && row >= Lk) {
-                    *(u32x4*)(dst + lane * 16) = u32x4{0u, 0u, 0u, 0u};
+            const char* src = isv ? Vh : Kh;
+            char* dst = smem + (isv ? G::kV : 0) + cc * 1024;
+            if (cc * 1024 + 1024 <= kv_bytes) {
+                __builtin_amdgcn_global_load_lds(src + byte, (lds_void_t*)dst, 16, 0, 0);
+            } else if (byte < BB) {
+                if (byte < kv_bytes) {
+                    __builtin_amdgcn_global_load_lds(src + byte, (lds_void_t*)dst, 16, 0, 0);
+                } else if (!isv) {
+                    const int col = (byte - kv_bytes) % (2 * D);
+                    __builtin_amdgcn_global_load_lds(src + (kv_bytes - 2 * D) + col, (lds_void_t*)dst,
+                                                     16, 0, 0);
                 } else {
-                    const size_t goff = (size_t)min(row, Lk - 1) * (2 * D) + col;
-                    __builtin_amdgcn_global_load_lds((isv ? Vh : Kh) + goff, (lds_void_t*)dst, 16, 0, 0);
+                    *(u32x4*)(dst + lane * 16) = u32x4{0u, 0u, 0u, 0u};
                 }
             }
         }
@@ -134,13 +139,13 @@ __global__ __launch_bounds__(W * 64) void attn_fwd_short_kernel(
         }
     }
 
-    // Constant block: a one in column 0 of every key row below Lk (the row-sum column).
+    // Row-sum column: V^T row D is read from a block with V's row stride whose
+    // first four columns hold (1, 0, 0, 0) for key rows below Lk and zeros past
+    // it; only those four columns are ever read.
     if constexpr (G::kOnes) {
-        const uint32_t one = from_float<ET>(1.0f);
-        for (int i = tid; i < BB / 16; i += kThreads) {
-            u32x4 w = {0u, 0u, 0u, 0u};
-            if ((i * 8) % D == 0 && (i * 8) / D < Lk) w[0] = one;
-            *(u32x4*)(smem + G::kC + i * 16) = w;
+        for (int r = tid; r < G::kRows; r += kThreads) {
+            u32x2 w = {r < Lk ? (uint32_t)from_float<ET>(1.0f) : 0u, 0u};
+            *(u32x2*)(smem + G::kC + r * (2 * D)) = w;
         }
     }
 
@@ -151,8 +156,10 @@ __global__ __launch_bounds__(W * 64) void attn_fwd_short_kernel(
         const int krow = 4 * (g >> 1) + (i >> 2);
 #pragma unroll
         for (int n = 0; n < DN; ++n) {
+            // rows past D + 3 of O^T are never used: those lanes read V
             const int ds = 32 * n + 16 * (g & 1) + 4 * (i & 3);
-            v_off[n] = ds < D ? G::kV + (krow * D + ds) * 2 : G::kC + (krow * D + ds - D) * 2;
+            v_off[n] = ds == D ? G::kC + krow * D * 2
+                               : G::kV + (krow * D + (ds < D ? ds : ds - 32)) * 2;
         }
     }
 
@@ -260,7 +267,7 @@ __global__ __launch_bounds__(W * 64) void attn_fwd_short_kernel(
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
             const int d0 = 32 * n + 8 * g + 4 * half;
-            if (d0 < D) {
+            if (32 * n + 8 * g < D) {   // D % 8 == 0: then d0 + 3 < D for both halves
                 u32x2 w;
                 w[0] = pack2<ET>(acc[n][4 * g + 0] * inv, acc[n][4 * g + 1] * inv);
                 w[1] = pack2<ET>(acc[n][4 * g + 2] * inv, acc[n][4 * g + 3] * inv);

@@ -1,24 +1,28 @@
 // attn_fwd.hip -- single-pass attention forward (Eq. 3) for gfx950, with the
 // K and V tiles streamed into LDS by direct global->LDS copies.
 //
-// One workgroup = 8 waves for 128 query rows of one (batch, head).  Waves
-// 0-3 take the first half of the key tiles and waves 4-7 the second half,
-// each wave owning 32 query rows; at the end the two halves of every row are
-// merged through LDS.  The key split gives four waves per SIMD (each at most
-// 128 VGPRs), which is what hides the latencies of the chain below.
+// One workgroup covers 128 query rows of one (batch, head).  Its waves are
+// split in two halves over the key tiles (the first half of the tiles and the
+// second), and at the end the two halves of every row are merged through LDS.
+// A wave owns QB blocks of 32 query rows: QB = 2 when D <= 64 (4 waves per
+// workgroup, two per SIMD, up to 256 VGPRs each), QB = 1 above (8 waves).
+// With QB = 2 every K and V^T operand read from LDS feeds two MFMAs.
 // Key/value tiles of 64 keys move through LDS double-buffered per half: while
 // one tile is consumed the next is copied straight from global memory
 // (global_load_lds, 16 bytes per lane, no registers involved), keeping the
-// row-major [key][d] layout.  Per 32-key sub-tile and wave:
+// row-major [key][d] layout.  Per 32-key sub-tile, wave and query block:
 //
 //   S^T = K Q^T      32x32x16 MFMA.  A = K rows read from LDS (16 bytes per
 //                    lane), B = Q^T held in registers for the whole kernel.
 //                    The accumulator puts one query per lane (lane % 32) and
 //                    16 of the 32 keys in that lane, so the row maximum needs a
 //                    single exchange between lane halves.
-//   p = 2^(c s - m)  c = |scale| log2(e); the running maximum m moves (with
-//                    the matching rescale of O and l) only when a sub-tile's
-//                    maximum exceeds it by more than 8, so p <= 256.
+//   p = 2^(c s - m)  c = |scale| log2(e).  m is fixed at the maximum of each
+//                    wave's first sub-tile (p may then exceed 1); a row whose
+//                    later logits would overflow the rounded p sends the
+//                    workgroup through an exact fallback in which m moves, with
+//                    the rescale of O and l, when a sub-tile's maximum exceeds
+//                    it by more than 8.
 //   O^T += V^T P^T   32x32x16 MFMA.  B = P straight from the S^T registers;
 //                    A = V^T, produced from the row-major V tile by the
 //                    transposing LDS read ds_read_b64_tr_b16: 16 lanes each
@@ -29,6 +33,10 @@
 //                    instead of V: a one at d = D and zeros beyond, so the P V
 //                    product also yields l in row D of O^T.  Otherwise the
 //                    packed p pairs are summed with v_dot2 against (1, 1).
+//
+// With the maximum fixed, a whole 64-key tile is software-pipelined so that
+// the exponentials run on the transcendental unit under the MFMAs of the
+// neighbouring steps (ordinary VALU work does not overlap the matrix core).
 //
 // This is the block-wise ("multi-stage") reduction of Sec. 3.2.1 -- a block's
 // maximum and exponential sum merged into the running pair, and the two key
@@ -42,10 +50,7 @@ namespace sdattn {
 
 namespace {
 
-constexpr int kQW = 4;                 // query waves, 32 rows each
-constexpr int kWaves = 2 * kQW;        // times two key halves
-constexpr int kThreads = kWaves * 64;
-constexpr int kBQ = kQW * 32;          // query rows per workgroup
+constexpr int kBQ = 128;               // query rows per workgroup
 constexpr int kKB = 64;                // keys per LDS tile
 constexpr float kRescaleSlack = 8.0f;
 constexpr int kMaxLds = 160 * 1024;
@@ -54,8 +59,16 @@ typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4_t;
 
+// QB = 32-row query blocks per wave.  With QB = 2 every K and V^T operand
+// read from LDS feeds two MFMAs (half the LDS traffic per flop) and each wave
+// carries two independent MFMA / softmax chains; the register budget is then
+// sized for two waves per SIMD.
 template <int D>
 struct Geom {
+    static constexpr int QB = D <= 64 ? 2 : 1;
+    static constexpr int kQW = 4 / QB;                        // query waves
+    static constexpr int kWaves = 2 * kQW;                    // times two key halves
+    static constexpr int kThreads = kWaves * 64;
     static constexpr int DK = (D + 15) / 16;                  // 16-deep k steps of Q K^T
     static constexpr int DN = (D + 31) / 32;                  // 32-row d tiles of O^T
     static constexpr bool kOnes = (D % 32) != 0;              // padding rows carry the row sum
@@ -63,12 +76,12 @@ struct Geom {
     static constexpr int kChunks = kTileBytes / 1024;         // 1 KiB wave copies per tile
     static constexpr int kBufBytes = kTileBytes * (kOnes ? 3 : 2);   // K, V (, constant block)
     static constexpr int kHalfBytes = 2 * kBufBytes;          // two buffers per key half
-    static constexpr int kMergeFloats = DN * 16 * 64 + 3 * 64;   // one wave's O^T, m, max, l
+    static constexpr int kMergeFloats = QB * (DN * 16 * 64 + 3 * 64);   // one wave's O^T, m, max, l
     static constexpr int kMergeBytes = kQW * kMergeFloats * 4;
     static constexpr int kLdsBytes = 2 * kHalfBytes > kMergeBytes ? 2 * kHalfBytes : kMergeBytes;
     static constexpr bool kFits = D >= 32 && D % 8 == 0 && kLdsBytes <= kMaxLds;
-    // waves per SIMD the register budget is sized for (4: 128 VGPRs each)
-    static constexpr int kWavesPerSimd = D <= 64 ? 4 : 2;
+    // waves per SIMD the register budget is sized for (2: 256 VGPRs each)
+    static constexpr int kWavesPerSimd = 2;
 };
 
 // Logical tile for workgroup `bid`.  Workgroups are dealt round-robin over the
@@ -86,13 +99,17 @@ __device__ __forceinline__ u32x2 lds_read_tr(const char* p) {
 }
 
 template <int ET, int D, bool STATS>
-__global__ __launch_bounds__(kThreads, Geom<D>::kWavesPerSimd) void attn_fwd_lds_kernel(
+__global__ __launch_bounds__(Geom<D>::kThreads, Geom<D>::kWavesPerSimd) void attn_fwd_lds_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     uint16_t* __restrict__ O, float* __restrict__ LS, int Lq, int Lk, float scale_abs, float c,
     int neg, int nqb) {
     using G = Geom<D>;
     constexpr int DK = G::DK;
     constexpr int DN = G::DN;
+    constexpr int QB = G::QB;
+    constexpr int kQW = G::kQW;
+    constexpr int kWaves = G::kWaves;
+    constexpr int kThreads = G::kThreads;
     constexpr int TB = G::kTileBytes;
 
     extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -108,7 +125,7 @@ __global__ __launch_bounds__(kThreads, Geom<D>::kWavesPerSimd) void attn_fwd_lds
     const int tile = xcd_remap(blockIdx.x, gridDim.x);
     const int bh = tile / nqb;
     const int qb = tile - bh * nqb;
-    const int q0 = qb * kBQ + wq * 32;
+    const int q0 = qb * kBQ + wq * 32 * QB;   // first row of this wave's QB blocks
 
     const char* Kh = (const char*)(K + (size_t)bh * Lk * D);
     const char* Vh = (const char*)(V + (size_t)bh * Lk * D);
@@ -133,40 +150,58 @@ __global__ __launch_bounds__(kThreads, Geom<D>::kWavesPerSimd) void attn_fwd_lds
     const int t_first = kh ? nh : 0;
     const int t_count = kh ? ntiles - nh : nh;
 
-    // Copy tile t of this half into its buffer b (the half's 4 waves issue
-    // the 1 KiB pieces wq, wq + 4, ...).  Rows past Lk repeat row Lk - 1
+    // Copy tile t of this half into its buffer b (the half's kQW waves issue
+    // the 1 KiB pieces wq, wq + kQW, ...).  Rows past Lk repeat row Lk - 1
     // (finite data; their weights are forced to zero).
     auto issue_tile = [&](int t, int b) __attribute__((always_inline)) {
         const int kbase = t * kKB;
-        const bool tail = kbase + kKB > Lk;
+        char* bufp = hbase + b * G::kBufBytes;
+        if (kbase + kKB <= Lk) {
+            // a full tile is one contiguous run of K (and of V) rows
+            const size_t tile_off = (size_t)kbase * (2 * D) + lane * 16;
 #pragma unroll
-        for (int i = 0; i < (2 * G::kChunks + kQW - 1) / kQW; ++i) {
-            const int cidx = wq + kQW * i;
-            if (cidx < 2 * G::kChunks) {
-                const bool isv = cidx >= G::kChunks;
-                const int cc = isv ? cidx - G::kChunks : cidx;
-                const int byte = cc * 1024 + lane * 16;
-                const int row = byte / (2 * D);
-                const int col = byte - row * (2 * D);
-                const int grow = tail ? min(kbase + row, Lk - 1) : kbase + row;
-                const size_t goff = (size_t)grow * (2 * D) + col;
-                char* dst = hbase + b * G::kBufBytes + (isv ? TB : 0) + cc * 1024;
-                __builtin_amdgcn_global_load_lds((isv ? Vh : Kh) + goff, (lds_void_t*)dst, 16, 0, 0);
+            for (int i = 0; i < (2 * G::kChunks + kQW - 1) / kQW; ++i) {
+                const int cidx = wq + kQW * i;
+                if (cidx < 2 * G::kChunks) {
+                    const bool isv = cidx >= G::kChunks;
+                    const int cc = isv ? cidx - G::kChunks : cidx;
+                    __builtin_amdgcn_global_load_lds((isv ? Vh : Kh) + tile_off + cc * 1024,
+                                                     (lds_void_t*)(bufp + (isv ? TB : 0) + cc * 1024),
+                                                     16, 0, 0);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < (2 * G::kChunks + kQW - 1) / kQW; ++i) {
+                const int cidx = wq + kQW * i;
+                if (cidx < 2 * G::kChunks) {
+                    const bool isv = cidx >= G::kChunks;
+                    const int cc = isv ? cidx - G::kChunks : cidx;
+                    const int byte = cc * 1024 + lane * 16;
+                    const int row = byte / (2 * D);
+                    const int col = byte - row * (2 * D);
+                    const size_t goff = (size_t)min(kbase + row, Lk - 1) * (2 * D) + col;
+                    __builtin_amdgcn_global_load_lds((isv ? Vh : Kh) + goff,
+                                                     (lds_void_t*)(bufp + (isv ? TB : 0) + cc * 1024),
+                                                     16, 0, 0);
+                }
             }
         }
     };
 
-    // Q^T operand: lane holds query q0 + l32, d = 16s + 8*half .. +7 for each s.
-    const int qrow = q0 + l32;
-    u32x4 qreg[DK];
+    // Q^T operand of block j: lane holds query q0 + 32j + l32, d = 16s + 8*half .. +7.
+    u32x4 qreg[QB][DK];
 #pragma unroll
-    for (int s = 0; s < DK; ++s) {
-        const int d0 = 16 * s + 8 * half;
-        u32x4 v = {0u, 0u, 0u, 0u};
-        if (qrow < Lq && d0 < D) v = *(const u32x4*)(Q + ((size_t)bh * Lq + qrow) * D + d0);
-        if (neg) v ^= 0x80008000u;   // fold a negative scale into Q (exact)
-        qreg[s] = v;
-    }
+    for (int j = 0; j < QB; ++j)
+#pragma unroll
+        for (int s = 0; s < DK; ++s) {
+            const int qrow = q0 + 32 * j + l32;
+            const int d0 = 16 * s + 8 * half;
+            u32x4 v = {0u, 0u, 0u, 0u};
+            if (qrow < Lq && d0 < D) v = *(const u32x4*)(Q + ((size_t)bh * Lq + qrow) * D + d0);
+            if (neg) v ^= 0x80008000u;   // fold a negative scale into Q (exact)
+            qreg[j][s] = v;
+        }
 
     // Per-lane LDS byte offsets inside a buffer.
     // K rows: lane reads key row l32 at d = 8*half (+16 s, +32 sub rows).
@@ -185,14 +220,23 @@ __global__ __launch_bounds__(kThreads, Geom<D>::kWavesPerSimd) void attn_fwd_lds
         }
     }
 
-    f32x16 acc[DN];
+    f32x16 acc[QB][DN];
+    float m_run[QB];   // running max used in the exponent (log2 units)
+    float s_max[QB];   // true running max of the raw scores
+    float l_part[QB];  // this lane's part of the row sum (v_dot2 path)
+    auto reset = [&]() __attribute__((always_inline)) {
 #pragma unroll
-    for (int n = 0; n < DN; ++n)
+        for (int j = 0; j < QB; ++j) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc[n][r] = 0.0f;
-    float m_run = -__builtin_inff();   // running max used in the exponent (log2 units)
-    float s_max = -__builtin_inff();   // true running max of the raw scores
-    float l_part = 0.0f;               // this lane's part of the row sum (v_dot2 path)
+            for (int n = 0; n < DN; ++n)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[j][n][r] = 0.0f;
+            m_run[j] = -__builtin_inff();
+            s_max[j] = -__builtin_inff();
+            l_part[j] = 0.0f;
+        }
+    };
+    reset();
 
     // How a sub-tile treats the running maximum m (log2 units):
     //   kFirst  the wave's first sub-tile: m = its row maximum (O is still 0)
@@ -209,67 +253,74 @@ __global__ __launch_bounds__(kThreads, Geom<D>::kWavesPerSimd) void attn_fwd_lds
                       __attribute__((always_inline)) {
         constexpr int MODE = decltype(mode_c)::value;
         constexpr bool TAIL = decltype(tail_c)::value;
-        // ---- S^T = K Q^T
-        f32x16 st;
+        // ---- S^T = K Q^T, one K operand read for the QB blocks
+        f32x16 st[QB];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) st[r] = 0.0f;
+        for (int j = 0; j < QB; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) st[j][r] = 0.0f;
 #pragma unroll
         for (int s = 0; s < DK; ++s) {
             const u32x4 a = *(const u32x4*)(buf + k_off + (32 * sub * D + 16 * s) * 2);
-            st = mfma32x32x16<ET>(a, qreg[s], st);
+#pragma unroll
+            for (int j = 0; j < QB; ++j) st[j] = mfma32x32x16<ET>(a, qreg[j][s], st[j]);
         }
-        if constexpr (TAIL) {
+        u32x4 pk[QB][2];
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int key = kbase + 8 * (r >> 2) + 4 * half + (r & 3);
-                if (key >= Lk) st[r] = -__builtin_inff();
-            }
-        }
-        // ---- row maximum (Eq. 4's L), where the mode needs it
-        if constexpr (MODE != kFixed || STATS) {
-            float mloc = st[0];
+        for (int j = 0; j < QB; ++j) {
+            if constexpr (TAIL) {
 #pragma unroll
-            for (int r = 1; r < 16; ++r) mloc = fmaxf(mloc, st[r]);
-            mloc = half_max(mloc);
-            s_max = fmaxf(s_max, mloc);
-            if constexpr (MODE == kFirst) {
-                m_run = mloc * c;
-            } else if constexpr (MODE == kOnline) {
-                const float mb = mloc * c;
-                if (__any(mb > m_run + kRescaleSlack)) {
-                    const float m_new = fmaxf(m_run, mb);
-                    const float alpha = fast_exp2(m_run - m_new);
-#pragma unroll
-                    for (int n = 0; n < DN; ++n)
-#pragma unroll
-                        for (int r = 0; r < 16; ++r) acc[n][r] *= alpha;
-                    l_part *= alpha;
-                    m_run = m_new;
+                for (int r = 0; r < 16; ++r) {
+                    const int key = kbase + 8 * (r >> 2) + 4 * half + (r & 3);
+                    if (key >= Lk) st[j][r] = -__builtin_inff();
                 }
             }
-        }
-        // ---- p = 2^(c s - m), rounded to the input type
-        const float negm = -m_run;
-        float p[16];
+            // ---- row maximum (Eq. 4's L), where the mode needs it
+            if constexpr (MODE != kFixed || STATS) {
+                float mloc = st[j][0];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) p[r] = fast_exp2(fmaf(st[r], c, negm));
-        if constexpr (TAIL) {
+                for (int r = 1; r < 16; ++r) mloc = fmaxf(mloc, st[j][r]);
+                mloc = half_max(mloc);
+                s_max[j] = fmaxf(s_max[j], mloc);
+                if constexpr (MODE == kFirst) {
+                    m_run[j] = mloc * c;
+                } else if constexpr (MODE == kOnline) {
+                    const float mb = mloc * c;
+                    if (__any(mb > m_run[j] + kRescaleSlack)) {
+                        const float m_new = fmaxf(m_run[j], mb);
+                        const float alpha = fast_exp2(m_run[j] - m_new);
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int key = kbase + 8 * (r >> 2) + 4 * half + (r & 3);
-                if (key >= Lk) p[r] = 0.0f;
+                        for (int n = 0; n < DN; ++n)
+#pragma unroll
+                            for (int r = 0; r < 16; ++r) acc[j][n][r] *= alpha;
+                        l_part[j] *= alpha;
+                        m_run[j] = m_new;
+                    }
+                }
             }
-        }
-        u32x4 pk[2];
+            // ---- p = 2^(c s - m), rounded to the input type
+            const float negm = -m_run[j];
+            float p[16];
 #pragma unroll
-        for (int u = 0; u < 2; ++u)
+            for (int r = 0; r < 16; ++r) p[r] = fast_exp2(fmaf(st[j][r], c, negm));
+            if constexpr (TAIL) {
 #pragma unroll
-            for (int w = 0; w < 4; ++w) pk[u][w] = pack2<ET>(p[8 * u + 2 * w], p[8 * u + 2 * w + 1]);
-        if constexpr (!G::kOnes) {
+                for (int r = 0; r < 16; ++r) {
+                    const int key = kbase + 8 * (r >> 2) + 4 * half + (r & 3);
+                    if (key >= Lk) p[r] = 0.0f;
+                }
+            }
 #pragma unroll
             for (int u = 0; u < 2; ++u)
 #pragma unroll
-                for (int w = 0; w < 4; ++w) l_part = add_pair<ET>(pk[u][w], l_part);
+                for (int w = 0; w < 4; ++w)
+                    pk[j][u][w] = pack2<ET>(p[8 * u + 2 * w], p[8 * u + 2 * w + 1]);
+            if constexpr (!G::kOnes) {
+#pragma unroll
+                for (int u = 0; u < 2; ++u)
+#pragma unroll
+                    for (int w = 0; w < 4; ++w) l_part[j] = add_pair<ET>(pk[j][u][w], l_part[j]);
+            }
         }
         // ---- O^T += V^T P^T; keys of operand slot e: 16u + 8*(e/4) + 4*half + e%4
 #pragma unroll
@@ -280,7 +331,8 @@ __global__ __launch_bounds__(kThreads, Geom<D>::kWavesPerSimd) void attn_fwd_lds
                 const u32x2 lo = lds_read_tr(vb);
                 const u32x2 hi = lds_read_tr(vb + 8 * D * 2);
                 const u32x4 a = {lo[0], lo[1], hi[0], hi[1]};
-                acc[n] = mfma32x32x16<ET>(a, pk[u], acc[n]);
+#pragma unroll
+                for (int j = 0; j < QB; ++j) acc[j][n] = mfma32x32x16<ET>(a, pk[j][u], acc[j][n]);
             }
     };
 
@@ -290,14 +342,113 @@ __global__ __launch_bounds__(kThreads, Geom<D>::kWavesPerSimd) void attn_fwd_lds
     std::integral_constant<int, kFixed> fixed_c;
     std::integral_constant<int, kOnline> online_c;
 
+    // A whole 64-key tile with the maximum fixed, scheduled as a software
+    // pipeline over the (sub-tile, block) pairs P0 = (0, 0), P1 = (0, 1), ...:
+    //   region 1        S^T of sub-tile 0
+    //   region 2        S^T of sub-tile 1   with the softmax of P0
+    //   region 2 + k    P V of P(k-1)       with the softmax of Pk
+    //   last region     P V of the last pair
+    // Hard scheduling fences separate the regions; inside one, each MFMA is
+    // followed by a share of the exponentials, so the transcendental unit
+    // runs under the matrix core.  (Plain VALU work -- the FMAs and
+    // conversions -- cannot overlap MFMAs and is left to the scheduler.)
+    auto tile_fixed = [&](const char* buf) __attribute__((always_inline)) {
+        constexpr int NP = 2 * QB;               // (sub-tile, block) pairs
+        f32x16 st[2][QB];
+        u32x4 pk[2][QB][2];
+        u32x4 vt[2][2][DN];
+        auto qk = [&](int sub) __attribute__((always_inline)) {
+#pragma unroll
+            for (int j = 0; j < QB; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) st[sub][j][r] = 0.0f;
+#pragma unroll
+            for (int s = 0; s < DK; ++s) {
+                const u32x4 a = *(const u32x4*)(buf + k_off + (32 * sub * D + 16 * s) * 2);
+#pragma unroll
+                for (int j = 0; j < QB; ++j) st[sub][j] = mfma32x32x16<ET>(a, qreg[j][s], st[sub][j]);
+            }
+        };
+        auto read_vt = [&](int sub) __attribute__((always_inline)) {
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+#pragma unroll
+                for (int n = 0; n < DN; ++n) {
+                    const char* vb = buf + v_off[n] + (32 * sub + 16 * u) * D * 2;
+                    const u32x2 lo = lds_read_tr(vb);
+                    const u32x2 hi = lds_read_tr(vb + 8 * D * 2);
+                    vt[sub][u][n] = u32x4{lo[0], lo[1], hi[0], hi[1]};
+                }
+        };
+        auto softmax = [&](int pr) __attribute__((always_inline)) {
+            const int sub = pr / QB, j = pr % QB;
+            float p[16];
+#pragma unroll
+            for (int r = 0; r < 16; ++r) p[r] = fast_exp2(fmaf(st[sub][j][r], c, -m_run[j]));
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+#pragma unroll
+                for (int w = 0; w < 4; ++w)
+                    pk[sub][j][u][w] = pack2<ET>(p[8 * u + 2 * w], p[8 * u + 2 * w + 1]);
+            if constexpr (!G::kOnes) {
+#pragma unroll
+                for (int u = 0; u < 2; ++u)
+#pragma unroll
+                    for (int w = 0; w < 4; ++w) l_part[j] = add_pair<ET>(pk[sub][j][u][w], l_part[j]);
+            }
+        };
+        auto pv = [&](int pr) __attribute__((always_inline)) {
+            const int sub = pr / QB, j = pr % QB;
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+#pragma unroll
+                for (int n = 0; n < DN; ++n) acc[j][n] = mfma32x32x16<ET>(vt[sub][u][n], pk[sub][j][u], acc[j][n]);
+        };
+        // each MFMA of a region followed by ceil(16 / MFMAs) exponentials
+        auto interleave = [&](auto nm_c) __attribute__((always_inline)) {
+            constexpr int NM = decltype(nm_c)::value;
+#pragma unroll
+            for (int i = 0; i < NM; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x400, (16 + NM - 1) / NM, 0);
+            }
+        };
+        std::integral_constant<int, DK * QB> nq_c;
+        std::integral_constant<int, 2 * DN> np_c;
+
+        qk(0);
+        __builtin_amdgcn_sched_barrier(0);
+        qk(1);
+        read_vt(0);
+        softmax(0);
+        interleave(nq_c);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int k = 1; k < NP; ++k) {
+            if (k == QB) read_vt(1);
+            pv(k - 1);
+            softmax(k);
+            interleave(np_c);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        if (QB == 1) read_vt(1);
+        pv(NP - 1);
+    };
+
     // consume the tile t (in buffer b) of this half; its first sub-tile in
     // mode mode0_c, the second in mode_c
     auto consume = [&](auto mode0_c, auto mode_c, int t, int b) __attribute__((always_inline)) {
         const char* buf = hbase + b * G::kBufBytes;
         const int kbase = t * kKB;
+        constexpr bool kPipelined = decltype(mode0_c)::value == kFixed &&
+                                    decltype(mode_c)::value == kFixed && !STATS;
         if (kbase + kKB <= Lk) {
-            step32(mode0_c, full_c, buf, 0, kbase);
-            step32(mode_c, full_c, buf, 1, kbase + 32);
+            if constexpr (kPipelined) {
+                tile_fixed(buf);
+            } else {
+                step32(mode0_c, full_c, buf, 0, kbase);
+                step32(mode_c, full_c, buf, 1, kbase + 32);
+            }
         } else {
             if (kbase + 32 <= Lk) step32(mode0_c, full_c, buf, 0, kbase);
             else step32(mode0_c, tail_c, buf, 0, kbase);
@@ -332,15 +483,19 @@ __global__ __launch_bounds__(kThreads, Geom<D>::kWavesPerSimd) void attn_fwd_lds
     // which makes this lane's row sum non-finite.  Any such row sends the
     // whole workgroup (it shares the LDS tiles) through the online path.
     {
-        float l_check;
-        if constexpr (G::kOnes) {
-            constexpr int dd = D % 32;
-            constexpr int rsel = 4 * (dd >> 3) + (dd & 3);
-            l_check = acc[D / 32][rsel];
-        } else {
-            l_check = l_part;
+        bool overflow = false;
+#pragma unroll
+        for (int j = 0; j < QB; ++j) {
+            float l_check;
+            if constexpr (G::kOnes) {
+                constexpr int dd = D % 32;
+                constexpr int rsel = 4 * (dd >> 3) + (dd & 3);
+                l_check = acc[j][D / 32][rsel];
+            } else {
+                l_check = l_part[j];
+            }
+            overflow = overflow || !(__builtin_fabsf(l_check) < __builtin_inff());
         }
-        const bool overflow = !(__builtin_fabsf(l_check) < __builtin_inff());
         // workgroup-wide OR through the (now idle) first LDS words
         int* vote = (int*)smem;
         const int wave_overflow = __any(overflow) ? 1 : 0;   // ballot with every lane active
@@ -351,75 +506,81 @@ __global__ __launch_bounds__(kThreads, Geom<D>::kWavesPerSimd) void attn_fwd_lds
         for (int w = 0; w < kWaves; ++w) any |= vote[w];
         __syncthreads();
         if (any) {
-#pragma unroll
-            for (int n = 0; n < DN; ++n)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) acc[n][r] = 0.0f;
-            m_run = -__builtin_inff();
-            s_max = -__builtin_inff();
-            l_part = 0.0f;
+            reset();
             run_tiles(online_c);
         }
     }
 
     // ---- merge the two key halves of every row (the block-merge rule)
+    constexpr int kMF = DN * 16 * 64 + 3 * 64;   // floats per query block
     float* mrg = (float*)smem + wq * G::kMergeFloats;
     if (kh == 1) {
 #pragma unroll
-        for (int n = 0; n < DN; ++n)
+        for (int j = 0; j < QB; ++j) {
+            float* mj = mrg + j * kMF;
 #pragma unroll
-            for (int r = 0; r < 16; ++r) mrg[(n * 16 + r) * 64 + lane] = acc[n][r];
-        mrg[DN * 16 * 64 + lane] = m_run;
-        mrg[DN * 16 * 64 + 64 + lane] = s_max;
-        mrg[DN * 16 * 64 + 128 + lane] = l_part;
+            for (int n = 0; n < DN; ++n)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) mj[(n * 16 + r) * 64 + lane] = acc[j][n][r];
+            mj[DN * 16 * 64 + lane] = m_run[j];
+            mj[DN * 16 * 64 + 64 + lane] = s_max[j];
+            mj[DN * 16 * 64 + 128 + lane] = l_part[j];
+        }
     }
     __syncthreads();
     if (kh == 1) return;
-    {
-        const float m_b = mrg[DN * 16 * 64 + lane];
-        const float m_new = fmaxf(m_run, m_b);
-        const float a0 = fast_exp2(m_run - m_new);   // exp2(-inf) = 0 for an empty half
+#pragma unroll
+    for (int j = 0; j < QB; ++j) {
+        const float* mj = mrg + j * kMF;
+        const float m_b = mj[DN * 16 * 64 + lane];
+        const float m_new = fmaxf(m_run[j], m_b);
+        const float a0 = fast_exp2(m_run[j] - m_new);   // exp2(-inf) = 0 for an empty half
         const float a1 = fast_exp2(m_b - m_new);
 #pragma unroll
         for (int n = 0; n < DN; ++n)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) acc[n][r] = acc[n][r] * a0 + mrg[(n * 16 + r) * 64 + lane] * a1;
-        s_max = fmaxf(s_max, mrg[DN * 16 * 64 + 64 + lane]);
-        l_part = l_part * a0 + mrg[DN * 16 * 64 + 128 + lane] * a1;
-        m_run = m_new;
+            for (int r = 0; r < 16; ++r)
+                acc[j][n][r] = acc[j][n][r] * a0 + mj[(n * 16 + r) * 64 + lane] * a1;
+        s_max[j] = fmaxf(s_max[j], mj[DN * 16 * 64 + 64 + lane]);
+        l_part[j] = l_part[j] * a0 + mj[DN * 16 * 64 + 128 + lane] * a1;
+        m_run[j] = m_new;
     }
 
     // ---- epilogue: l, O / l, store
-    float l;
-    if constexpr (G::kOnes) {
-        constexpr int dd = D % 32;               // position of the ones row in its d tile
-        constexpr int hsel = (dd >> 2) & 1, rsel = 4 * (dd >> 3) + (dd & 3);
-        const float own = acc[D / 32][rsel];
-        const float other = half_partner(own, half);
-        l = (half == hsel) ? own : other;
-    } else {
-        l = half_sum(l_part);
-    }
-    const float inv = 1.0f / l;
-    if (qrow < Lq) {
-        uint16_t* orow = O + ((size_t)bh * Lq + qrow) * D;
 #pragma unroll
-        for (int n = 0; n < DN; ++n)
+    for (int j = 0; j < QB; ++j) {
+        float l;
+        if constexpr (G::kOnes) {
+            constexpr int dd = D % 32;               // position of the ones row in its d tile
+            constexpr int hsel = (dd >> 2) & 1, rsel = 4 * (dd >> 3) + (dd & 3);
+            const float own = acc[j][D / 32][rsel];
+            const float other = half_partner(own, half);
+            l = (half == hsel) ? own : other;
+        } else {
+            l = half_sum(l_part[j]);
+        }
+        const float inv = 1.0f / l;
+        const int qrow = q0 + 32 * j + l32;
+        if (qrow < Lq) {
+            uint16_t* orow = O + ((size_t)bh * Lq + qrow) * D;
 #pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                const int d0 = 32 * n + 8 * g + 4 * half;
-                if (d0 < D) {
-                    u32x2 w;
-                    w[0] = pack2<ET>(acc[n][4 * g + 0] * inv, acc[n][4 * g + 1] * inv);
-                    w[1] = pack2<ET>(acc[n][4 * g + 2] * inv, acc[n][4 * g + 3] * inv);
-                    *(u32x2*)(orow + d0) = w;
+            for (int n = 0; n < DN; ++n)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int d0 = 32 * n + 8 * g + 4 * half;
+                    if (32 * n + 8 * g < D) {   // D % 8 == 0: then d0 + 3 < D for both halves
+                        u32x2 w;
+                        w[0] = pack2<ET>(acc[j][n][4 * g + 0] * inv, acc[j][n][4 * g + 1] * inv);
+                        w[1] = pack2<ET>(acc[j][n][4 * g + 2] * inv, acc[j][n][4 * g + 3] * inv);
+                        *(u32x2*)(orow + d0) = w;
+                    }
                 }
+            if (LS && half == 0) {
+                // Eq. 4 in natural units: L = max_j scale q.k, S = sum_j exp(scale q.k - L)
+                float* o2 = LS + ((size_t)bh * Lq + qrow) * 2;
+                o2[0] = s_max[j] * scale_abs;
+                o2[1] = l * fast_exp2(m_run[j] - s_max[j] * c);
             }
-        if (LS && half == 0) {
-            // Eq. 4 in natural units: L = max_j scale q.k, S = sum_j exp(scale q.k - L)
-            float* o2 = LS + ((size_t)bh * Lq + qrow) * 2;
-            o2[0] = s_max * scale_abs;
-            o2[1] = l * fast_exp2(m_run - s_max * c);
         }
     }
 }
@@ -443,7 +604,7 @@ hipError_t launch_d(const AttnArgs& a) {
         if (attr0 != hipSuccess) return attr0;
         if (attr1 != hipSuccess) return attr1;
         auto kern = a.ls ? attn_fwd_lds_kernel<ET, D, true> : attn_fwd_lds_kernel<ET, D, false>;
-        hipLaunchKernelGGL(kern, dim3((unsigned)nblk), dim3(kThreads),
+        hipLaunchKernelGGL(kern, dim3((unsigned)nblk), dim3(G::kThreads),
                            G::kLdsBytes, (hipStream_t)a.stream, (const uint16_t*)a.q,
                            (const uint16_t*)a.k, (const uint16_t*)a.v, (uint16_t*)a.out, a.ls,
                            a.Lq, a.Lk, scale_abs, c, a.scale < 0 ? 1 : 0, nqb);

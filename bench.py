@@ -109,7 +109,7 @@ def main():
 
     self_tflops = self_case.flops / (self_ms * 1e-3) / 1e12
     roofline = {
-        "kernel": "attn_fwd_kernel (self-attention, D=40)",
+        "kernel": "attn_fwd_lds_kernel<f16, D=40> (self-attention)",
         "bound": "mfma",
         "achieved": round(self_tflops, 2),
         "peak": PEAK_F16_TFLOPS,
@@ -142,10 +142,16 @@ def main():
         "self_attention": {"avg_kernel_us": round(self_ms * 1e3, 3), "tflops": round(self_tflops, 2),
                            "frac_f16_peak": round(self_tflops / PEAK_F16_TFLOPS, 4)},
     }
-    cross_gbs = cross_case.bytes / (cross_ms * 1e-3) / 1e9
-    out["cross"] = {"avg_kernel_us": round(cross_ms * 1e3, 3), "bytes_per_launch": cross_case.bytes,
+    # The cross-attention kernel lasts a few microseconds, so an event pair
+    # around each launch also times the dispatch gap the events themselves
+    # create; its duration is taken from back-to-back launches instead, with
+    # events only around the batch (the in-step event figure is kept too).
+    warm_ms = back_to_back_ms(torch, sd, stream, [(cq, ck, cv, co)], cross_case.scale)
+    cross_gbs = cross_case.bytes / (warm_ms * 1e-3) / 1e9
+    out["cross"] = {"avg_kernel_us": round(warm_ms * 1e3, 3), "bytes_per_launch": cross_case.bytes,
                     "warm_gbs": round(cross_gbs, 1), "warm_frac_hbm": round(cross_gbs / PEAK_HBM_GBS, 4),
-                    "tflops": round(cross_case.flops / (cross_ms * 1e-3) / 1e12, 2)}
+                    "tflops": round(cross_case.flops / (warm_ms * 1e-3) / 1e12, 2),
+                    "in_step_event_us": round(cross_ms * 1e3, 3)}
 
     if not args.no_extras:
         out["cross"].update(cold_cross(torch, sd, wl, dev, stream, cross_case))
@@ -160,33 +166,39 @@ def main():
     print(json.dumps(out), flush=True)
 
 
-def cold_cross(torch, sd, wl, dev, stream, case, nsets=40, reps=3):
+def back_to_back_ms(torch, sd, stream, sets, scale, launches=200, reps=3):
+    """Mean duration of one launch over `launches` back-to-back calls cycling through
+    `sets`, queued behind a busy GPU so the events time the kernels, not the host."""
+    for s in sets:
+        sd.forward(*s, scale, stream)
+    torch.cuda.synchronize()
+    best = None
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(20_000_000)
+        e0.record(stream)
+        for i in range(launches):
+            sd.forward(*sets[i % len(sets)], scale, stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / launches
+        best = ms if best is None else min(best, ms)
+    return best
+
+
+def cold_cross(torch, sd, wl, dev, stream, case, nsets=40):
     """Cross-attention with inputs rotated over nsets buffers (> 256 MiB in total)."""
     sets = []
     for i in range(nsets):
         q, k, v = wl.make_qkv(case.B, case.H, case.Lq, case.Lk, case.D, case.seed + 100 + i)
         qd, kd, vd = (torch.from_numpy(t).to(dev) for t in (q, k, v))
         sets.append((qd, kd, vd, torch.empty_like(qd)))
-    for s in sets:
-        sd.forward(*s, case.scale, stream)
-    torch.cuda.synchronize()
-    times = []
-    for _ in range(reps):
-        evs = [torch.cuda.Event(enable_timing=True) for _ in range(nsets + 1)]
-        # keep the GPU busy while the launches are queued, so the events time
-        # back-to-back kernels rather than the host's launch rate
-        torch.cuda._sleep(20_000_000)
-        evs[0].record(stream)
-        for i, s in enumerate(sets):
-            sd.forward(*s, case.scale, stream)
-            evs[i + 1].record(stream)
-        torch.cuda.synchronize()
-        times += [evs[i].elapsed_time(evs[i + 1]) for i in range(nsets)]
-    ms = float(np.mean(times))
+    ms = back_to_back_ms(torch, sd, stream, sets, case.scale, launches=5 * nsets)
     gbs = case.bytes / (ms * 1e-3) / 1e9
     return {"cold_avg_kernel_us": round(ms * 1e3, 3), "cold_gbs": round(gbs, 1),
             "cold_frac_hbm": round(gbs / PEAK_HBM_GBS, 4),
-            "cold_protocol": f"{nsets} input sets of {case.bytes} B rotated ({nsets * case.bytes / 2**20:.0f} MiB)"}
+            "cold_protocol": f"{nsets} input sets of {case.bytes} B rotated ({nsets * case.bytes / 2**20:.0f} MiB), "
+                             "back-to-back launches"}
 
 
 def bench_softmax_rows(torch, sd, dev, stream, reps=10):

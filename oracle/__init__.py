@@ -11,6 +11,9 @@ passages of the paper each function follows):
   normalise times V), returning O and Eq. 4's L and S.
 * :func:`softmax_rows` -- Eq. 4's reduction (L, S) on a given matrix and the
   element-wise step p = exp(a - L) / S.
+* :func:`logits` and :func:`softmax_pv` -- the first and last steps of the
+  partially fused softmax (Sec. 3.2.1): A = scale Q K^T, and
+  O = exp(A - L) / S times V.
 
 Inputs are numpy arrays: float16, float32, float64, or bfloat16 passed as a
 uint16 bit-pattern array with ``dtype="bf16"``.
@@ -39,6 +42,12 @@ def _load():
         lib.oracle_attention_f64.restype = i32
         lib.oracle_softmax_rows_f64.argtypes = [vp, i32, i64, i64, f32, i32, vp, vp]
         lib.oracle_softmax_rows_f64.restype = i32
+        lib.oracle_logits_f64.argtypes = [vp, vp, i32, i32, i32, i32, i32, i32, f32, vp, i64,
+                                          i32, vp]
+        lib.oracle_logits_f64.restype = i32
+        lib.oracle_softmax_pv_f64.argtypes = [vp, i32, vp, vp, i32, i32, i32, i32, i32, i32,
+                                              vp, i64, i32, vp]
+        lib.oracle_softmax_pv_f64.restype = i32
         lib.oracle_widen.argtypes = [vp, i32, i64, vp]
         lib.oracle_widen.restype = i32
         lib.oracle_num_threads.argtypes = [i32]
@@ -128,3 +137,57 @@ def softmax_rows(a, scale=1.0, want_p=False, dtype=None, nthreads=0):
     if want_p:
         return ls[:, 0], ls[:, 1], p
     return ls[:, 0], ls[:, 1]
+
+
+def _rows_arg(rows, total):
+    if rows is None:
+        return total, None, None
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    return rows.size, rows, _ptr(rows)
+
+
+def logits(q, k, scale, rows=None, dtype=None, nthreads=0):
+    """A = scale * Q K^T in fp64 for q [B,H,Lq,D], k [B,H,Lk,D].
+
+    Returns [B,H,Lq,Lk] (or [len(rows), Lk] for the flat query rows listed).
+    """
+    q, k = np.ascontiguousarray(q), np.ascontiguousarray(k)
+    if q.ndim != 4 or k.ndim != 4 or q.shape[:2] != k.shape[:2] or q.shape[3] != k.shape[3]:
+        raise ValueError("expected q [B,H,Lq,D] and k [B,H,Lk,D]")
+    if q.dtype != k.dtype:
+        raise TypeError("q and k must share one element type")
+    B, H, Lq, D = q.shape
+    Lk = k.shape[2]
+    n, rows, rp = _rows_arg(rows, B * H * Lq)
+    out = np.empty((n, Lk), dtype=np.float64)
+    rc = _load().oracle_logits_f64(_ptr(q), _ptr(k), _code(q, dtype), B, H, Lq, Lk, D,
+                                   float(np.float32(scale)), rp, n, int(nthreads), _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle_logits_f64 rejected its arguments")
+    return out.reshape(B, H, Lq, Lk) if rows is None else out
+
+
+def softmax_pv(a, v, ls=None, rows=None, a_dtype=None, v_dtype=None, nthreads=0):
+    """O = exp(A - L) / S times V in fp64, for a [B,H,Lq,Lk] (scale applied) and v [B,H,Lk,D].
+
+    ls: optional [B,H,Lq,2] (L, S) to use; None computes Eq. 4 from A.
+    Returns [B,H,Lq,D] (or [len(rows), D]).
+    """
+    a, v = np.ascontiguousarray(a), np.ascontiguousarray(v)
+    if a.ndim != 4 or v.ndim != 4 or a.shape[:2] != v.shape[:2] or a.shape[3] != v.shape[2]:
+        raise ValueError("expected a [B,H,Lq,Lk] and v [B,H,Lk,D]")
+    B, H, Lq, Lk = a.shape
+    D = v.shape[3]
+    lsp = None
+    if ls is not None:
+        ls = np.ascontiguousarray(ls, dtype=np.float64)
+        if ls.size != B * H * Lq * 2:
+            raise ValueError("ls must hold (L, S) for every row")
+        lsp = _ptr(ls)
+    n, rows, rp = _rows_arg(rows, B * H * Lq)
+    out = np.empty((n, D), dtype=np.float64)
+    rc = _load().oracle_softmax_pv_f64(_ptr(a), _code(a, a_dtype), lsp, _ptr(v), _code(v, v_dtype),
+                                       B, H, Lq, Lk, D, rp, n, int(nthreads), _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle_softmax_pv_f64 rejected its arguments")
+    return out.reshape(B, H, Lq, D) if rows is None else out

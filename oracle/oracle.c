@@ -205,3 +205,102 @@ int oracle_softmax_rows_f64(const void *a, int dtype, int64_t rows, int64_t cols
     }
     return 0;
 }
+
+/*
+ * The partially fused softmax of Sec. 3.2.1 splits Eq. 3 into three steps:
+ * the logit matrix, Eq. 4's reduction (oracle_softmax_rows_f64 above), and
+ * the element-wise normalisation fused with the product by V.  The first and
+ * last steps follow.
+ *
+ * Logits: out[t][j] = scale * <q_i, k_j> for the query row r = (b*H + h)*Lq + i
+ * (all B*H*Lq rows when `rows` is NULL, else the `nrows` rows listed), Q
+ * [B,H,Lq,D] and K [B,H,Lk,D] of element type `dtype`.  out: [n][Lk] doubles.
+ */
+int oracle_logits_f64(const void *q, const void *k, int dtype, int B, int H, int Lq, int Lk,
+                      int D, float scale, const int64_t *rows, int64_t nrows, int nthreads,
+                      double *out)
+{
+    if (!q || !k || !out || B < 1 || H < 1 || Lq < 1 || Lk < 1 || D < 1 ||
+        dtype < OR_F16 || dtype > OR_F64)
+        return 1;
+    const int64_t total = (int64_t)B * H * Lq;
+    const int64_t n = rows ? nrows : total;
+    if (n < 0)
+        return 1;
+    if (rows)
+        for (int64_t t = 0; t < n; ++t)
+            if (rows[t] < 0 || rows[t] >= total)
+                return 1;
+    const double sc = (double)scale;
+
+#pragma omp parallel for schedule(static) num_threads(oracle_num_threads(nthreads))
+    for (int64_t t = 0; t < n; ++t) {
+        const int64_t r = rows ? rows[t] : t;
+        const int64_t qrow = r * D;
+        const int64_t k0 = (r / Lq) * Lk * D;
+        for (int j = 0; j < Lk; ++j) {
+            double dot = 0.0;
+            for (int d = 0; d < D; ++d)
+                dot += or_elem(q, dtype, qrow + d) * or_elem(k, dtype, k0 + (int64_t)j * D + d);
+            out[t * Lk + j] = sc * dot;
+        }
+    }
+    return 0;
+}
+
+/*
+ * Normalise and multiply by V: for each selected row r of the logit matrix A
+ * [B,H,Lq,Lk] (element type a_dtype, the scale already applied) and V
+ * [B,H,Lk,D] (element type v_dtype),
+ *   o[t][d] = sum_j exp(a_rj - L_r) / S_r * v_jd,
+ * with (L_r, S_r) = ls[2r], ls[2r+1] when `ls` is given ([B*H*Lq][2]
+ * doubles), else Eq. 4 computed from A's row: L_r = max_j a_rj,
+ * S_r = sum_j exp(a_rj - L_r).  out: [n][D] doubles.
+ */
+int oracle_softmax_pv_f64(const void *a, int a_dtype, const double *ls, const void *v,
+                          int v_dtype, int B, int H, int Lq, int Lk, int D, const int64_t *rows,
+                          int64_t nrows, int nthreads, double *out)
+{
+    if (!a || !v || !out || B < 1 || H < 1 || Lq < 1 || Lk < 1 || D < 1 ||
+        a_dtype < OR_F16 || a_dtype > OR_F64 || v_dtype < OR_F16 || v_dtype > OR_F64)
+        return 1;
+    const int64_t total = (int64_t)B * H * Lq;
+    const int64_t n = rows ? nrows : total;
+    if (n < 0)
+        return 1;
+    if (rows)
+        for (int64_t t = 0; t < n; ++t)
+            if (rows[t] < 0 || rows[t] >= total)
+                return 1;
+
+#pragma omp parallel for schedule(static) num_threads(oracle_num_threads(nthreads))
+    for (int64_t t = 0; t < n; ++t) {
+        const int64_t r = rows ? rows[t] : t;
+        const int64_t arow = r * Lk;
+        const int64_t v0 = (r / Lq) * Lk * D;
+        double Lr, Sr;
+        if (ls) {
+            Lr = ls[2 * r];
+            Sr = ls[2 * r + 1];
+        } else {
+            Lr = -INFINITY;
+            for (int j = 0; j < Lk; ++j) {
+                const double x = or_elem(a, a_dtype, arow + j);
+                if (x > Lr)
+                    Lr = x;
+            }
+            Sr = 0.0;
+            for (int j = 0; j < Lk; ++j)
+                Sr += exp(or_elem(a, a_dtype, arow + j) - Lr);
+        }
+        double *o = out + t * D;
+        for (int d = 0; d < D; ++d)
+            o[d] = 0.0;
+        for (int j = 0; j < Lk; ++j) {
+            const double pij = exp(or_elem(a, a_dtype, arow + j) - Lr) / Sr;
+            for (int d = 0; d < D; ++d)
+                o[d] += pij * or_elem(v, v_dtype, v0 + (int64_t)j * D + d);
+        }
+    }
+    return 0;
+}

@@ -355,3 +355,111 @@ def test_sweep_has_sixteen_blocks_of_self_and_cross():
     assert sides == [4096] * 2 + [1024] * 2 + [256] * 2 + [64] + [256] * 3 + [1024] * 3 + [4096] * 3
     assert all(c.Lk == 77 for c in cases[1::2])
     assert len({c.seed for s in range(20) for c in wl.sweep_cases(s)}) == 640
+
+
+# ------------------------------------------- partially fused softmax steps
+# (Sec. 3.2.1: logits A = scale Q K^T, Eq. 4's reduction, then exp(A - L)/S
+# times V.)  Pins: numpy's fp64 matmul for the logits, a 50-digit brute force
+# of the last step on a given A, the composition identity with the pinned
+# attention, closed forms, and the roles of L and S when they are passed in.
+
+def test_logits_match_numpy_fp64_matmul():
+    rng = np.random.default_rng(40)
+    q = _rand16(rng, (2, 3, 17, 40))
+    k = _rand16(rng, (2, 3, 29, 40))
+    a = oracle.logits(q, k, 0.375)
+    ref = 0.375 * np.matmul(q.astype(np.float64), np.swapaxes(k.astype(np.float64), 2, 3))
+    assert a.shape == (2, 3, 17, 29)
+    assert np.max(np.abs(a - ref)) <= 1e-13 * np.abs(ref).max()
+    # a transposed operand or a swapped head would not match
+    assert np.max(np.abs(a[0, 1] - a[0, 2])) > 1.0
+
+
+def test_logits_rows_subset_and_bf16():
+    rng = np.random.default_rng(41)
+    q, k, _ = wl.make_qkv(1, 2, 9, 11, 16, 42, dtype="bf16")
+    a = oracle.logits(q, k, 0.25, dtype="bf16")
+    qf, kf = oracle.widen(q, dtype="bf16"), oracle.widen(k, dtype="bf16")
+    ref = 0.25 * np.matmul(qf, np.swapaxes(kf, 2, 3))
+    assert np.max(np.abs(a - ref)) <= 1e-13 * np.abs(ref).max()
+    rows = np.array([0, 8, 9, 17])
+    sub = oracle.logits(q, k, 0.25, rows=rows, dtype="bf16")
+    assert np.array_equal(sub, a.reshape(-1, 11)[rows])
+
+
+def _brute_force_pv(a, v):
+    """sum_j e^{a_j} v_j / sum_j e^{a_j} at 50 digits, no max shift."""
+    mp = mpmath.mp
+    mp.dps = 50
+    B, H, Lq, Lk = a.shape
+    D = v.shape[3]
+    out = np.zeros((B, H, Lq, D))
+    for b in range(B):
+        for h in range(H):
+            for i in range(Lq):
+                w = [mpmath.exp(mpmath.mpf(float(x))) for x in a[b, h, i]]
+                tot = mpmath.fsum(w)
+                for d in range(D):
+                    out[b, h, i, d] = float(mpmath.fsum(w[j] * mpmath.mpf(float(v[b, h, j, d]))
+                                                        for j in range(Lk)) / tot)
+    return out
+
+
+@pytest.mark.parametrize("a_scale", [1.0, 40.0])
+def test_softmax_pv_brute_force_small(a_scale):
+    rng = np.random.default_rng(43)
+    a = (rng.standard_normal((1, 2, 4, 9)) * a_scale).astype(np.float32)   # logits up to ~100
+    v = _rand16(rng, (1, 2, 9, 8))
+    o = oracle.softmax_pv(a, v)
+    ref = _brute_force_pv(a, v)
+    assert np.max(np.abs(o - ref)) <= 1e-12 * np.abs(v.astype(np.float64)).max()
+
+
+def test_logits_then_softmax_pv_is_attention():
+    q, k, v = wl.make_qkv(2, 2, 33, 47, 24, 44)
+    scale = float(np.float32(1 / np.sqrt(24)))
+    a = oracle.logits(q, k, scale)
+    o = oracle.softmax_pv(a, v)
+    r, _, _ = oracle.attention(q, k, v, scale)
+    assert np.max(np.abs(o - r)) <= 1e-13
+    # with Eq. 4's statistics taken from softmax_rows on the same A
+    L, S = oracle.softmax_rows(a.reshape(-1, 47))
+    o2 = oracle.softmax_pv(a, v, ls=np.stack([L, S], axis=1))
+    assert np.max(np.abs(o2 - r)) <= 1e-13
+
+
+def test_softmax_pv_closed_forms():
+    rng = np.random.default_rng(45)
+    v = _rand16(rng, (1, 2, 13, 16))
+    vf = v.astype(np.float64)
+    # constant rows of A: uniform weights, the mean of V
+    a = np.broadcast_to(rng.standard_normal((1, 2, 6, 1)), (1, 2, 6, 13)).copy()
+    o = oracle.softmax_pv(a, v)
+    assert np.max(np.abs(o - vf.mean(axis=2, keepdims=True))) <= 1e-14
+    # one logit 60 above the rest (other weights < 1e-25): that value row
+    a = rng.standard_normal((1, 2, 6, 13))
+    star = rng.integers(0, 13, size=(2, 6))
+    for h in range(2):
+        for i in range(6):
+            a[0, h, i, star[h, i]] = 60.0
+    o = oracle.softmax_pv(a, v)
+    for h in range(2):
+        for i in range(6):
+            assert np.max(np.abs(o[0, h, i] - vf[0, h, star[h, i]])) <= 1e-15
+
+
+def test_softmax_pv_uses_the_given_l_and_s():
+    rng = np.random.default_rng(46)
+    a = rng.standard_normal((1, 1, 5, 12))
+    v = _rand16(rng, (1, 1, 12, 8))
+    L, S = oracle.softmax_rows(a.reshape(-1, 12))
+    base = oracle.softmax_pv(a, v, ls=np.stack([L, S], axis=1))
+    # (L + c, S e^{-c}) is the same normalisation: the result does not move
+    c = 3.5
+    same = oracle.softmax_pv(a, v, ls=np.stack([L + c, S * np.exp(-c)], axis=1))
+    assert np.max(np.abs(same - base)) <= 1e-14
+    # doubling S halves O; lowering L by 1 scales O by e
+    half = oracle.softmax_pv(a, v, ls=np.stack([L, 2 * S], axis=1))
+    assert np.max(np.abs(half - base / 2)) <= 1e-15
+    up = oracle.softmax_pv(a, v, ls=np.stack([L - 1, S], axis=1))
+    assert np.max(np.abs(up - base * np.e)) <= 1e-14

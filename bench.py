@@ -156,6 +156,7 @@ def main():
     if not args.no_extras:
         out["cross"].update(cold_cross(torch, sd, wl, dev, stream, cross_case))
         out["softmax_rows"] = bench_softmax_rows(torch, sd, dev, stream)
+        out["two_pass"] = bench_two_pass(torch, sd, stream, self_case, (sq, sk, sv), self_ms)
 
     if args.copy_calibration:
         out["copy_calibration"] = copy_calibration(torch, dev, stream)
@@ -199,6 +200,47 @@ def cold_cross(torch, sd, wl, dev, stream, case, nsets=40):
             "cold_frac_hbm": round(gbs / PEAK_HBM_GBS, 4),
             "cold_protocol": f"{nsets} input sets of {case.bytes} B rotated ({nsets * case.bytes / 2**20:.0f} MiB), "
                              "back-to-back launches"}
+
+
+def bench_two_pass(torch, sd, stream, case, qkv, fused_ms, reps=5):
+    """The partially fused softmax as three launches at the 64x64 level (logits
+    in fp16 -> Eq. 4's (L, S) -> exp/normalise times V), against the fused kernel."""
+    q, k, v = qkv
+    B, H, Lq, Lk, D = case.B, case.H, case.Lq, case.Lk, case.D
+    a = torch.empty(B, H, Lq, Lk, dtype=torch.float16, device=q.device)
+    ls = torch.empty(B, H, Lq, 2, dtype=torch.float32, device=q.device)
+    o = torch.empty_like(q)
+    a2, ls2 = a.view(B * H * Lq, Lk), ls.view(B * H * Lq, 2)
+    calls = [lambda: sd.logits(q, k, a, case.scale, stream),
+             lambda: sd.softmax_rows(a2, ls2, None, 1.0, stream),
+             lambda: sd.softmax_pv(a, ls, v, o, stream)]
+    for c in calls:
+        c()
+    torch.cuda.synchronize()
+    t = [[] for _ in calls]
+    for _ in range(reps):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)]
+        ev[0].record(stream)
+        for i, c in enumerate(calls):
+            c()
+            ev[i + 1].record(stream)
+        torch.cuda.synchronize()
+        for i in range(len(calls)):
+            t[i].append(ev[i].elapsed_time(ev[i + 1]))
+    ms = [float(np.median(x)) for x in t]
+    a_bytes = a.numel() * 2
+    qkv_bytes = 2 * B * H * D * 2 * (Lq + Lk)
+    total = sum(ms)
+    return {
+        "logits_us": round(ms[0] * 1e3, 2), "logits_gbs": round((a_bytes + qkv_bytes / 2) / (ms[0] * 1e-3) / 1e9, 1),
+        "softmax_rows_us": round(ms[1] * 1e3, 2), "softmax_rows_gbs": round(a_bytes / (ms[1] * 1e-3) / 1e9, 1),
+        "softmax_pv_us": round(ms[2] * 1e3, 2), "softmax_pv_gbs": round((a_bytes + qkv_bytes / 2) / (ms[2] * 1e-3) / 1e9, 1),
+        "total_us": round(total * 1e3, 2),
+        "fused_us": round(fused_ms * 1e3, 2),
+        "fused_speedup": round(total / fused_ms, 2),
+        "a_bytes": a_bytes,
+        "config": "self B2 H8 L4096 D40, logits stored in fp16 (537 MB, written once, read twice)",
+    }
 
 
 def bench_softmax_rows(torch, sd, dev, stream, reps=10):

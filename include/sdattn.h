@@ -50,7 +50,7 @@ typedef enum {
 typedef enum {
     SDATTN_F16 = 0,              /* IEEE binary16 */
     SDATTN_BF16 = 1,             /* bfloat16 */
-    SDATTN_F32 = 2               /* IEEE binary32 (sdattn_softmax_rows input only) */
+    SDATTN_F32 = 2               /* IEEE binary32 (logit matrices only) */
 } sdattn_dtype;
 
 /*
@@ -98,6 +98,42 @@ int sdattn_forward_ex(const void *q, const void *k, const void *v, void *out, fl
  */
 int sdattn_softmax_rows(const void *a, float *ls, void *p, long long rows, long long cols,
                         float scale, sdattn_dtype dtype, void *stream);
+
+/*
+ * The partially fused softmax of Sec. 3.2.1 as separate launches: the logit
+ * matrix A = scale Q K^T is written to memory, Eq. 4's (L, S) is taken per
+ * row with sdattn_softmax_rows (A viewed as [B*H*Lq, Lk], scale 1), and the
+ * element-wise normalisation exp(a_ij - L_i) / S_i is fused with the product
+ * by V.  The three calls compute Eq. 3 (the rounding of A aside) and let the
+ * caller compare the method with the single-pass sdattn_forward.
+ *
+ * Logits:
+ *   q   [B, H, Lq, D] of `dtype` (fp16 or bf16)
+ *   k   [B, H, Lk, D] of `dtype`
+ *   a   [B, H, Lq, Lk] of `a_dtype` (fp16, bf16 or fp32):
+ *       a[b,h,i,j] = scale * q_i . k_j, accumulated in fp32, rounded to nearest even
+ *
+ * Requirements: q, k, a 16-byte aligned; B, H, Lq, Lk >= 1; 8 <= D <= 256
+ * with D % 8 == 0; finite scale; a must not overlap q or k.
+ */
+int sdattn_logits(const void *q, const void *k, void *a, int B, int H, int Lq, int Lk, int D,
+                  float scale, sdattn_dtype dtype, sdattn_dtype a_dtype, void *stream);
+
+/*
+ * Normalise and multiply by V:
+ *   a   [B, H, Lq, Lk] of `a_dtype` (fp16, bf16 or fp32), the scale already applied
+ *   ls  fp32 [B, H, Lq, 2]: (L_i, S_i) of each row of a, as sdattn_softmax_rows writes them
+ *   v   [B, H, Lk, D] of `dtype` (fp16 or bf16)
+ *   out [B, H, Lq, D] of `dtype`: out[b,h,i,:] = sum_j exp(a_ij - L_i) / S_i * v_j
+ *
+ * p = exp(a_ij - L_i) is rounded to `dtype` before the product with V, as in
+ * sdattn_forward; S_i is used as given.  Requirements: a, v, out 16-byte
+ * aligned, ls 8-byte aligned; sizes as for sdattn_logits; out must not
+ * overlap a, ls or v.  Fastest when Lk % 8 == 0.
+ */
+int sdattn_softmax_pv(const void *a, const float *ls, const void *v, void *out, int B, int H,
+                      int Lq, int Lk, int D, sdattn_dtype a_dtype, sdattn_dtype dtype,
+                      void *stream);
 
 /* Static English text for a status code (never NULL). */
 const char *sdattn_status_str(int status);

@@ -7,7 +7,7 @@ library is loaded on first use; if it is missing the call raises instead of
 falling back to anything else.
 """
 from .binding import (  # noqa: F401
-    SdattnError, forward, forward_ex, softmax_rows, library_path, load_library,
+    SdattnError, forward, forward_ex, softmax_rows, logits, softmax_pv, library_path, load_library,
     STATUS_OK, STATUS_INVALID_ARG, STATUS_UNSUPPORTED, STATUS_MISALIGNED, STATUS_HIP,
     DTYPE_F16, DTYPE_BF16, DTYPE_F32,
 )

@@ -26,8 +26,8 @@ DTYPE_BF16 = 1
 DTYPE_F32 = 2
 
 # every symbol include/sdattn.h declares
-EXPORTS = ("sdattn_forward", "sdattn_forward_ex", "sdattn_softmax_rows",
-           "sdattn_status_str", "sdattn_last_hip_error", "sdattn_version")
+EXPORTS = ("sdattn_forward", "sdattn_forward_ex", "sdattn_softmax_rows", "sdattn_logits",
+           "sdattn_softmax_pv", "sdattn_status_str", "sdattn_last_hip_error", "sdattn_version")
 
 _lib = None
 
@@ -60,6 +60,10 @@ def load_library():
     lib.sdattn_forward_ex.restype = i32
     lib.sdattn_softmax_rows.argtypes = [vp, vp, vp, i64, i64, f32, i32, vp]
     lib.sdattn_softmax_rows.restype = i32
+    lib.sdattn_logits.argtypes = [vp, vp, vp, i32, i32, i32, i32, i32, f32, i32, i32, vp]
+    lib.sdattn_logits.restype = i32
+    lib.sdattn_softmax_pv.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, vp]
+    lib.sdattn_softmax_pv.restype = i32
     lib.sdattn_status_str.argtypes = [i32]
     lib.sdattn_status_str.restype = ctypes.c_char_p
     lib.sdattn_last_hip_error.argtypes = []
@@ -135,3 +139,25 @@ def softmax_rows(a, ls, p=None, scale: float = 1.0, stream=None):
         _dtype_code(a), _stream(stream))
     _check("sdattn_softmax_rows", status)
     return ls
+
+
+def logits(q, k, a, scale: float, stream=None):
+    """a = scale * q k^T: q [B,H,Lq,D], k [B,H,Lk,D] (fp16/bf16), a [B,H,Lq,Lk] (fp16/bf16/fp32)."""
+    B, H, Lq, D = q.shape
+    Lk = k.shape[2]
+    status = load_library().sdattn_logits(
+        _dev(q, "q"), _dev(k, "k"), _dev(a, "a"), B, H, Lq, Lk, D, ctypes.c_float(scale),
+        _dtype_code(q), _dtype_code(a), _stream(stream))
+    _check("sdattn_logits", status)
+    return a
+
+
+def softmax_pv(a, ls, v, out, stream=None):
+    """out = exp(a - L) / S times v, with (L, S) = ls [B,H,Lq,2] fp32 of a's rows."""
+    B, H, Lq, Lk = a.shape
+    D = v.shape[3]
+    status = load_library().sdattn_softmax_pv(
+        _dev(a, "a"), _dev(ls, "ls"), _dev(v, "v"), _dev(out, "out"), B, H, Lq, Lk, D,
+        _dtype_code(a), _dtype_code(v), _stream(stream))
+    _check("sdattn_softmax_pv", status)
+    return out

@@ -39,4 +39,30 @@ struct SoftmaxArgs {
 
 hipError_t launch_softmax_rows(const SoftmaxArgs& a);
 
+// The first and last steps of the partially fused softmax (twopass.hip).
+struct LogitsArgs {
+    const void* q;
+    const void* k;
+    void* a;        // [B,H,Lq,Lk] of a_dtype
+    int B, H, Lq, Lk, D;
+    float scale;
+    int dtype;      // Q, K: kF16 or kBF16
+    int a_dtype;    // kF16, kBF16 or kF32
+    void* stream;
+};
+long long logits_grid(int B, int H, int Lq, int Lk);
+hipError_t launch_logits(const LogitsArgs& a);
+
+struct SoftmaxPvArgs {
+    const void* a;  // [B,H,Lq,Lk] of a_dtype
+    const float* ls;   // [B,H,Lq,2] (L, S) of A's rows
+    const void* v;
+    void* out;
+    int B, H, Lq, Lk, D;
+    int dtype;      // V, out: kF16 or kBF16
+    int a_dtype;    // kF16, kBF16 or kF32
+    void* stream;
+};
+hipError_t launch_softmax_pv(const SoftmaxPvArgs& a);
+
 }  // namespace sdattn

@@ -77,6 +77,34 @@ int run_attention(const void* q, const void* k, const void* v, void* out, float*
     return finish(sdattn::launch_attn_fwd(a));
 }
 
+int elem_size(int dtype) {
+    switch (dtype) {
+        case SDATTN_F16:
+        case SDATTN_BF16: return 2;
+        case SDATTN_F32: return 4;
+        default: return 0;
+    }
+}
+
+// Shared checks of sdattn_logits and sdattn_softmax_pv: sizes, types, and the
+// element counts of the [B,H,Lq,D], [B,H,Lk,D] and [B,H,Lq,Lk] tensors.
+int check_twopass(int B, int H, int Lq, int Lk, int D, int dtype, int a_dtype, long long* nq,
+                  long long* nk, long long* na) {
+    if (B < 1 || H < 1 || Lq < 1 || Lk < 1 || D < 1) return SDATTN_ERR_INVALID_ARG;
+    if (dtype != SDATTN_F16 && dtype != SDATTN_BF16) {
+        return dtype == SDATTN_F32 ? SDATTN_ERR_UNSUPPORTED : SDATTN_ERR_INVALID_ARG;
+    }
+    if (elem_size(a_dtype) == 0) return SDATTN_ERR_INVALID_ARG;
+    if (D % 8 != 0 || D > 256) return SDATTN_ERR_UNSUPPORTED;
+    *nq = checked_mul({B, H, Lq, D});
+    *nk = checked_mul({B, H, Lk, D});
+    *na = checked_mul({B, H, Lq, Lk, elem_size(a_dtype)});
+    if (*nq < 0 || *nk < 0 || *na < 0) return SDATTN_ERR_UNSUPPORTED;
+    if (sdattn::logits_grid(B, H, Lq, Lk) > INT_MAX || sdattn::attn_fwd_grid(B, H, Lq) > INT_MAX)
+        return SDATTN_ERR_UNSUPPORTED;
+    return SDATTN_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -112,6 +140,36 @@ int sdattn_softmax_rows(const void* a, float* ls, void* p, long long rows, long 
     (void)hipGetLastError();
     sdattn::SoftmaxArgs args{a, ls, p, rows, cols, scale, (int)dtype, stream};
     return finish(sdattn::launch_softmax_rows(args));
+}
+
+int sdattn_logits(const void* q, const void* k, void* a, int B, int H, int Lq, int Lk, int D,
+                  float scale, sdattn_dtype dtype, sdattn_dtype a_dtype, void* stream) {
+    if (!q || !k || !a) return SDATTN_ERR_INVALID_ARG;
+    if (!isfinite(scale)) return SDATTN_ERR_INVALID_ARG;
+    long long nq, nk, na;
+    const int st = check_twopass(B, H, Lq, Lk, D, (int)dtype, (int)a_dtype, &nq, &nk, &na);
+    if (st != SDATTN_OK) return st;
+    if (!aligned(q, 16) || !aligned(k, 16) || !aligned(a, 16)) return SDATTN_ERR_MISALIGNED;
+    if (overlap(a, na, q, 2ULL * nq) || overlap(a, na, k, 2ULL * nk)) return SDATTN_ERR_INVALID_ARG;
+    (void)hipGetLastError();
+    sdattn::LogitsArgs args{q, k, a, B, H, Lq, Lk, D, scale, (int)dtype, (int)a_dtype, stream};
+    return finish(sdattn::launch_logits(args));
+}
+
+int sdattn_softmax_pv(const void* a, const float* ls, const void* v, void* out, int B, int H,
+                      int Lq, int Lk, int D, sdattn_dtype a_dtype, sdattn_dtype dtype, void* stream) {
+    if (!a || !ls || !v || !out) return SDATTN_ERR_INVALID_ARG;
+    long long nq, nk, na;
+    const int st = check_twopass(B, H, Lq, Lk, D, (int)dtype, (int)a_dtype, &nq, &nk, &na);
+    if (st != SDATTN_OK) return st;
+    if (!aligned(a, 16) || !aligned(v, 16) || !aligned(out, 16) || !aligned(ls, 8))
+        return SDATTN_ERR_MISALIGNED;
+    const unsigned long long ob = 2ULL * nq, lb = 8ULL * (unsigned long long)(nq / D);
+    if (overlap(out, ob, a, na) || overlap(out, ob, ls, lb) || overlap(out, ob, v, 2ULL * nk))
+        return SDATTN_ERR_INVALID_ARG;
+    (void)hipGetLastError();
+    sdattn::SoftmaxPvArgs args{a, ls, v, out, B, H, Lq, Lk, D, (int)dtype, (int)a_dtype, stream};
+    return finish(sdattn::launch_softmax_pv(args));
 }
 
 const char* sdattn_status_str(int status) {

@@ -141,3 +141,40 @@ def test_binding_raises_when_library_missing(monkeypatch, tmp_path):
     monkeypatch.setenv("SDATTN_LIBRARY", str(tmp_path / "absent.so"))
     with pytest.raises(RuntimeError, match="not built"):
         binding.load_library()
+
+
+def lg(lib, q=QA, k=KA, a=OA, B=2, H=8, Lq=64, Lk=77, D=40, scale=0.158, dtype=F16, a_dtype=F16):
+    return lib.sdattn_logits(q, k, a, B, H, Lq, Lk, D, ctypes.c_float(scale), dtype, a_dtype, None)
+
+
+def pv(lib, a=QA, ls=LA, v=VA, o=OA, B=2, H=8, Lq=64, Lk=77, D=40, a_dtype=F16, dtype=F16):
+    return lib.sdattn_softmax_pv(a, ls, v, o, B, H, Lq, Lk, D, a_dtype, dtype, None)
+
+
+def test_logits_checks(lib):
+    for field in ("q", "k", "a"):
+        assert lg(lib, **{field: None}) == INVALID
+    for field in ("B", "H", "Lq", "Lk", "D"):
+        assert lg(lib, **{field: 0}) == INVALID
+    assert lg(lib, scale=float("nan")) == INVALID
+    assert lg(lib, dtype=F32) == UNSUPPORTED
+    assert lg(lib, a_dtype=9) == INVALID
+    assert lg(lib, D=44) == UNSUPPORTED
+    assert lg(lib, B=1 << 20, H=1 << 20, Lq=1 << 12, Lk=1 << 12) == UNSUPPORTED
+    assert lg(lib, a=ctypes.c_void_p(0x40000000 + 8)) == MISALIGNED
+    assert lg(lib, a=ctypes.c_void_p(0x20000000 - 64)) == INVALID        # a's tail runs into k
+    assert lg(lib, a=ctypes.c_void_p(0x10000000 + 4096), a_dtype=F32) == INVALID   # inside q
+
+
+def test_softmax_pv_checks(lib):
+    for field in ("a", "ls", "v", "o"):
+        assert pv(lib, **{field: None}) == INVALID
+    for field in ("B", "H", "Lq", "Lk", "D"):
+        assert pv(lib, **{field: -1}) == INVALID
+    assert pv(lib, dtype=F32) == UNSUPPORTED
+    assert pv(lib, a_dtype=5) == INVALID
+    assert pv(lib, D=300) == UNSUPPORTED
+    assert pv(lib, ls=ctypes.c_void_p(0x50000004)) == MISALIGNED
+    assert pv(lib, v=ctypes.c_void_p(0x30000008)) == MISALIGNED
+    assert pv(lib, o=ctypes.c_void_p(0x10000000 + 1024)) == INVALID      # out inside a
+    assert pv(lib, o=ctypes.c_void_p(0x50000000 - 64)) == INVALID        # out's tail runs into ls

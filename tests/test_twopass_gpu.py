@@ -200,3 +200,25 @@ def test_chain_bf16():
     out, _ = gpu_chain(q, k, v, scale, "f32", dtype="bf16")
     r, _, _ = oracle.attention(q, k, v, scale, dtype="bf16")
     assert_close(to_host64(out), r, "bf16", what="bf16 chain")
+
+
+@pytest.mark.parametrize("Lk", [8, 64, 72, 136, 264])
+def test_softmax_pv_uneven_key_halves_after_nan_lds(Lk):
+    """Key counts whose tiles split unevenly between the two wave halves (or
+    leave the second half none), run right after a kernel that left NaN in LDS:
+    a half must not multiply p = 0 by a V buffer it never filled."""
+    import torch
+    nan = np.full((2, 8, 512, 64), np.nan, dtype=np.float16)
+    nd = torch.from_numpy(nan).cuda()
+    sd.forward(nd, nd, nd, torch.empty_like(nd), 0.125)   # K/V tiles of NaN in LDS
+    B, H, Lq, D = 2, 4, 300, 40
+    rng = np.random.default_rng(5500 + Lk)
+    a = (rng.standard_normal((B, H, Lq, Lk), dtype=np.float32) * np.float32(2.0)).astype(np.float16)
+    _, _, v = wl.make_qkv(B, H, 1, Lk, D, 5600 + Lk)
+    ad = torch.from_numpy(a).cuda()
+    ls = torch.empty(B, H, Lq, 2, dtype=torch.float32, device="cuda")
+    sd.softmax_rows(ad.view(-1, Lk), ls.view(-1, 2), None, scale=1.0)
+    out = torch.empty(B, H, Lq, D, dtype=torch.float16, device="cuda")
+    sd.softmax_pv(ad, ls, to_device(v), out)
+    torch.cuda.synchronize()
+    assert_close(to_host64(out), oracle.softmax_pv(a, v), what=f"Lk={Lk}")

@@ -14,6 +14,8 @@ passages of the paper each function follows):
 * :func:`logits` and :func:`softmax_pv` -- the first and last steps of the
   partially fused softmax (Sec. 3.2.1): A = scale Q K^T, and
   O = exp(A - L) / S times V.
+* :func:`linear` and :func:`attention_block` -- the projections around the
+  attention in SD's transformer blocks and the whole multi-head block.
 
 Inputs are numpy arrays: float16, float32, float64, or bfloat16 passed as a
 uint16 bit-pattern array with ``dtype="bf16"``.
@@ -48,6 +50,11 @@ def _load():
         lib.oracle_softmax_pv_f64.argtypes = [vp, i32, vp, vp, i32, i32, i32, i32, i32, i32,
                                               vp, i64, i32, vp]
         lib.oracle_softmax_pv_f64.restype = i32
+        lib.oracle_linear_f64.argtypes = [vp, i32, vp, i32, vp, i64, i32, i32, i32, vp]
+        lib.oracle_linear_f64.restype = i32
+        lib.oracle_attention_block_f64.argtypes = [vp, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32,
+                                                   i32, i32, i32, f32, vp, i64, i32, vp]
+        lib.oracle_attention_block_f64.restype = i32
         lib.oracle_widen.argtypes = [vp, i32, i64, vp]
         lib.oracle_widen.restype = i32
         lib.oracle_num_threads.argtypes = [i32]
@@ -191,3 +198,55 @@ def softmax_pv(a, v, ls=None, rows=None, a_dtype=None, v_dtype=None, nthreads=0)
     if rc != 0:
         raise ValueError("oracle_softmax_pv_f64 rejected its arguments")
     return out.reshape(B, H, Lq, D) if rows is None else out
+
+
+def linear(x, w, bias=None, dtype=None, nthreads=0):
+    """y = x w^T + bias in fp64: x [..., K], w [N, K] (out, in), bias [N] like w.
+
+    Returns [..., N].
+    """
+    x, w = np.ascontiguousarray(x), np.ascontiguousarray(w)
+    K = x.shape[-1]
+    if w.ndim != 2 or w.shape[1] != K:
+        raise ValueError("expected x [..., K] and w [N, K]")
+    N = w.shape[0]
+    M = x.size // K
+    bp = None
+    if bias is not None:
+        bias = np.ascontiguousarray(bias)
+        if bias.shape != (N,) or bias.dtype != w.dtype:
+            raise ValueError("bias must be [N] of w's type")
+        bp = _ptr(bias)
+    y = np.empty((M, N), dtype=np.float64)
+    rc = _load().oracle_linear_f64(_ptr(x), _code(x, dtype), _ptr(w), _code(w, dtype), bp, M, K, N,
+                                   int(nthreads), _ptr(y))
+    if rc != 0:
+        raise ValueError("oracle_linear_f64 rejected its arguments")
+    return y.reshape(x.shape[:-1] + (N,))
+
+
+def attention_block(x, ctx, wq, wk, wv, wo, bo, heads, scale, rows=None, dtype=None, nthreads=0):
+    """SD's multi-head attention block in fp64 (see oracle.c): x [B,Lq,C], ctx [B,Lk,Cc],
+    weights [out, in], bo [C] (or None).  Returns [B,Lq,C] (or [len(rows), C] for the
+    flat rows b*Lq + i listed)."""
+    arrs = [np.ascontiguousarray(t) for t in (x, ctx, wq, wk, wv, wo)]
+    x, ctx, wq, wk, wv, wo = arrs
+    if len({a.dtype for a in arrs}) != 1:
+        raise TypeError("all tensors must share one element type")
+    B, Lq, C = x.shape
+    Lk, Cc = ctx.shape[1], ctx.shape[2]
+    if wq.shape != (C, C) or wk.shape != (C, Cc) or wv.shape != (C, Cc) or wo.shape != (C, C):
+        raise ValueError("weight shapes do not match x and ctx")
+    bp = None
+    if bo is not None:
+        bo = np.ascontiguousarray(bo)
+        bp = _ptr(bo)
+    n, rows, rp = _rows_arg(rows, B * Lq)
+    out = np.empty((n, C), dtype=np.float64)
+    rc = _load().oracle_attention_block_f64(_ptr(x), _ptr(ctx), _ptr(wq), _ptr(wk), _ptr(wv),
+                                            _ptr(wo), bp, _code(x, dtype), B, Lq, Lk, C, Cc,
+                                            int(heads), float(np.float32(scale)), rp, n,
+                                            int(nthreads), _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle_attention_block_f64 rejected its arguments")
+    return out.reshape(B, Lq, C) if rows is None else out

@@ -304,3 +304,137 @@ int oracle_softmax_pv_f64(const void *a, int a_dtype, const double *ls, const vo
     }
     return 0;
 }
+
+/*
+ * The steps either side of the attention in SD's UNet transformer blocks:
+ * a linear layer, and the attention block built from them.
+ *
+ * Linear layer with weights stored [out, in]:
+ *   y[m][n] = sum_k x[m][k] * w[n][k] + bias[n]   (bias may be NULL)
+ * x [M][K] of x_dtype, w [N][K] of w_dtype, bias [N] of w_dtype; y [M][N] doubles.
+ */
+int oracle_linear_f64(const void *x, int x_dtype, const void *w, int w_dtype, const void *bias,
+                      int64_t M, int K, int N, int nthreads, double *y)
+{
+    if (!x || !w || !y || M < 1 || K < 1 || N < 1 || x_dtype < OR_F16 || x_dtype > OR_F64 ||
+        w_dtype < OR_F16 || w_dtype > OR_F64)
+        return 1;
+
+#pragma omp parallel for schedule(static) num_threads(oracle_num_threads(nthreads))
+    for (int64_t m = 0; m < M; ++m) {
+        for (int n = 0; n < N; ++n) {
+            double acc = 0.0;
+            for (int k = 0; k < K; ++k)
+                acc += or_elem(x, x_dtype, m * K + k) * or_elem(w, w_dtype, (int64_t)n * K + k);
+            y[m * N + n] = acc + (bias ? or_elem(bias, w_dtype, n) : 0.0);
+        }
+    }
+    return 0;
+}
+
+/*
+ * The attention block (multi-head attention over Eq. 3), all tensors of one
+ * element type `dtype`:
+ *   x   [B][Lq][C]   latent tokens          ctx [B][Lk][Cc]  context tokens
+ *   wq  [C][C], wk [C][Cc], wv [C][Cc], wo [C][C]  (weights [out, in]); bo [C]
+ *   Q = x wq^T, K = ctx wk^T, V = ctx wv^T, each split into H heads of D = C/H
+ *   channels (head h holds channels h*D .. h*D + D - 1);
+ *   O_h = softmax(scale Q_h K_h^T) V_h per head (Eq. 3);
+ *   out = [O_0 | O_1 | ... | O_{H-1}] wo^T + bo.
+ * Q, K, V and O stay in fp64 between the steps.  rows: NULL for all B*Lq
+ * rows, else `nrows` flat rows b*Lq + i.  out: [n][C] doubles.
+ */
+int oracle_attention_block_f64(const void *x, const void *ctx, const void *wq, const void *wk,
+                               const void *wv, const void *wo, const void *bo, int dtype, int B,
+                               int Lq, int Lk, int C, int Cc, int H, float scale,
+                               const int64_t *rows, int64_t nrows, int nthreads, double *out)
+{
+    if (!x || !ctx || !wq || !wk || !wv || !wo || !out || B < 1 || Lq < 1 || Lk < 1 || C < 1 ||
+        Cc < 1 || H < 1 || C % H != 0 || dtype < OR_F16 || dtype > OR_F64)
+        return 1;
+    const int D = C / H;
+    const int64_t total = (int64_t)B * Lq;
+    const int64_t n = rows ? nrows : total;
+    if (n < 0)
+        return 1;
+    if (rows)
+        for (int64_t t = 0; t < n; ++t)
+            if (rows[t] < 0 || rows[t] >= total)
+                return 1;
+    /* K and V of every context token: [B][Lk][C] each */
+    double *Kf = (double *)malloc(sizeof(double) * (size_t)B * Lk * C);
+    double *Vf = (double *)malloc(sizeof(double) * (size_t)B * Lk * C);
+    if (!Kf || !Vf) {
+        free(Kf);
+        free(Vf);
+        return 1;
+    }
+    if (oracle_linear_f64(ctx, dtype, wk, dtype, NULL, (int64_t)B * Lk, Cc, C, nthreads, Kf) ||
+        oracle_linear_f64(ctx, dtype, wv, dtype, NULL, (int64_t)B * Lk, Cc, C, nthreads, Vf)) {
+        free(Kf);
+        free(Vf);
+        return 1;
+    }
+    const double sc = (double)scale;
+    int bad = 0;
+
+#pragma omp parallel num_threads(oracle_num_threads(nthreads)) reduction(| : bad)
+    {
+        double *q = (double *)malloc(sizeof(double) * (size_t)C);
+        double *o = (double *)malloc(sizeof(double) * (size_t)C);
+        double *a = (double *)malloc(sizeof(double) * (size_t)Lk);
+        if (!q || !o || !a) {
+            bad = 1;
+        } else {
+#pragma omp for schedule(static)
+            for (int64_t t = 0; t < n; ++t) {
+                const int64_t r = rows ? rows[t] : t;
+                const int64_t b = r / Lq;
+                /* q = x_r wq^T */
+                for (int c = 0; c < C; ++c) {
+                    double acc = 0.0;
+                    for (int k = 0; k < C; ++k)
+                        acc += or_elem(x, dtype, r * C + k) * or_elem(wq, dtype, (int64_t)c * C + k);
+                    q[c] = acc;
+                }
+                /* each head: Eq. 3 in three passes (max, exp-sum, normalise times V) */
+                for (int h = 0; h < H; ++h) {
+                    double Lh = -INFINITY;
+                    for (int j = 0; j < Lk; ++j) {
+                        const double *kj = Kf + ((size_t)b * Lk + j) * C + (size_t)h * D;
+                        double dot = 0.0;
+                        for (int d = 0; d < D; ++d)
+                            dot += q[h * D + d] * kj[d];
+                        a[j] = sc * dot;
+                        if (a[j] > Lh)
+                            Lh = a[j];
+                    }
+                    double Sh = 0.0;
+                    for (int j = 0; j < Lk; ++j)
+                        Sh += exp(a[j] - Lh);
+                    for (int d = 0; d < D; ++d)
+                        o[h * D + d] = 0.0;
+                    for (int j = 0; j < Lk; ++j) {
+                        const double pij = exp(a[j] - Lh) / Sh;
+                        const double *vj = Vf + ((size_t)b * Lk + j) * C + (size_t)h * D;
+                        for (int d = 0; d < D; ++d)
+                            o[h * D + d] += pij * vj[d];
+                    }
+                }
+                /* out = o wo^T + bo */
+                for (int c = 0; c < C; ++c) {
+                    double acc = 0.0;
+                    for (int k = 0; k < C; ++k)
+                        acc += o[k] * or_elem(wo, dtype, (int64_t)c * C + k);
+                    out[t * C + c] = acc + (bo ? or_elem(bo, dtype, c) : 0.0);
+                }
+            }
+        }
+        free(q);
+        free(o);
+        free(a);
+    }
+    free(Kf);
+    free(Vf);
+    return bad;
+}

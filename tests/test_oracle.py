@@ -463,3 +463,71 @@ def test_softmax_pv_uses_the_given_l_and_s():
     assert np.max(np.abs(half - base / 2)) <= 1e-15
     up = oracle.softmax_pv(a, v, ls=np.stack([L - 1, S], axis=1))
     assert np.max(np.abs(up - base * np.e)) <= 1e-14
+
+
+# ------------------------------------------------- projections and the block
+# Pins: numpy's fp64 matmul for the linear layer; torch's fp64 CPU
+# scaled_dot_product_attention composed with torch matmuls (an independent
+# library) for the multi-head block; closed forms (zero value or output
+# weights leave the bias; one head is the single-head attention of the
+# projections); row subsets.
+
+def _blk_inputs(seed, B=2, Lq=9, Lk=7, C=32, Cc=24, dtype=np.float16):
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((B, Lq, C)).astype(dtype)
+    ctx = rng.standard_normal((B, Lk, Cc)).astype(dtype)
+    ws = [(rng.standard_normal(s) / np.sqrt(s[1])).astype(dtype)
+          for s in ((C, C), (C, Cc), (C, Cc), (C, C))]
+    bo = (rng.standard_normal(C) * 0.5).astype(dtype)
+    return x, ctx, ws, bo
+
+
+def test_linear_matches_numpy_matmul():
+    rng = np.random.default_rng(60)
+    x = _rand16(rng, (3, 5, 40))
+    w = _rand16(rng, (24, 40))
+    b = _rand16(rng, (24,))
+    y = oracle.linear(x, w, b)
+    ref = x.astype(np.float64) @ w.astype(np.float64).T + b.astype(np.float64)
+    assert y.shape == (3, 5, 24)
+    assert np.max(np.abs(y - ref)) <= 1e-13 * np.abs(ref).max()
+    assert np.max(np.abs(oracle.linear(x, w) - (ref - b.astype(np.float64)))) <= 1e-13 * np.abs(ref).max()
+
+
+def test_attention_block_matches_torch_fp64():
+    torch = pytest.importorskip("torch")
+    x, ctx, (wq, wk, wv, wo), bo = _blk_inputs(61)
+    H, scale = 4, float(np.float32(0.3))   # the oracle takes the scale as fp32
+    out = oracle.attention_block(x, ctx, wq, wk, wv, wo, bo, H, scale)
+    t = lambda a: torch.from_numpy(a.astype(np.float64))
+    B, Lq, C = x.shape
+    Lk = ctx.shape[1]
+    q = (t(x) @ t(wq).T).view(B, Lq, H, C // H).transpose(1, 2)
+    k = (t(ctx) @ t(wk).T).view(B, Lk, H, C // H).transpose(1, 2)
+    v = (t(ctx) @ t(wv).T).view(B, Lk, H, C // H).transpose(1, 2)
+    o = torch.nn.functional.scaled_dot_product_attention(q, k, v, scale=scale)
+    ref = (o.transpose(1, 2).reshape(B, Lq, C) @ t(wo).T + t(bo)).numpy()
+    assert np.max(np.abs(out - ref)) <= 1e-12 * max(1.0, np.abs(ref).max())
+
+
+def test_attention_block_closed_forms():
+    x, ctx, (wq, wk, wv, wo), bo = _blk_inputs(62)
+    z = np.zeros_like(wo)
+    bf = bo.astype(np.float64)
+    assert np.max(np.abs(oracle.attention_block(x, ctx, wq, wk, wv, z, bo, 4, 0.3) - bf)) == 0.0
+    assert np.max(np.abs(oracle.attention_block(x, ctx, wq, wk, np.zeros_like(wv), wo, bo, 4, 0.3)
+                         - bf)) <= 1e-15
+    # one head: the single-head attention of the fp64 projections, then wo
+    out1 = oracle.attention_block(x, ctx, wq, wk, wv, wo, None, 1, 0.3)
+    q, k, v = (oracle.linear(a, w)[:, None] for a, w in ((x, wq), (ctx, wk), (ctx, wv)))
+    o, _, _ = oracle.attention(q, k, v, 0.3)
+    ref = oracle.linear(o[:, 0], wo)
+    assert np.max(np.abs(out1 - ref)) <= 1e-13
+
+
+def test_attention_block_rows_subset():
+    x, ctx, (wq, wk, wv, wo), bo = _blk_inputs(63)
+    full = oracle.attention_block(x, ctx, wq, wk, wv, wo, bo, 2, 0.25)
+    rows = np.array([0, 3, 8, 9, 17])
+    sub = oracle.attention_block(x, ctx, wq, wk, wv, wo, bo, 2, 0.25, rows=rows)
+    assert np.array_equal(sub, full.reshape(-1, full.shape[-1])[rows])

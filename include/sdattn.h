@@ -135,6 +135,62 @@ int sdattn_softmax_pv(const void *a, const float *ls, const void *v, void *out, 
                       int Lq, int Lk, int D, sdattn_dtype a_dtype, sdattn_dtype dtype,
                       void *stream);
 
+/*
+ * The steps either side of Eq. 3 in SD's transformer blocks: the Q, K, V and
+ * output projections, and the split of their channels into heads.  A tensor
+ * of token rows (B batches x L tokens, C channels) is stored in one of two
+ * layouts:
+ *   SDATTN_ROWS   [B, L, C]
+ *   SDATTN_HEADS  [B, H, L, C/H]: channel c = h*(C/H) + d of token l at
+ *                 ((b*H + h)*L + l)*(C/H) + d -- the layout the attention
+ *                 entry points take, so a projection written in it is the
+ *                 head split, and one read from it is the head merge.
+ */
+typedef enum {
+    SDATTN_ROWS = 0,
+    SDATTN_HEADS = 1
+} sdattn_layout;
+
+/*
+ * Linear layer with weights stored [out, in]:
+ *   y[m, n] = sum_k x[m, k] * w[n, k] + bias[n]     for the B*L token rows m = b*L + l
+ *
+ *   x     token rows of K channels in `x_layout`, `dtype` (fp16 or bf16)
+ *   w     [N, K] of `dtype`; bias [N] of `dtype` or NULL
+ *   y     token rows of N channels in `y_layout`, `dtype`, accumulated in fp32
+ *         and rounded to nearest even
+ *   H     heads of a SDATTN_HEADS side (ignored when neither side uses it)
+ *
+ * Requirements: x, w, y 16-byte aligned; B, L, K, N >= 1; K % 8 == 0 and
+ * N % 8 == 0; on a SDATTN_HEADS side H >= 1 divides that side's channels into
+ * widths that are multiples of 8; y must not overlap x, w or bias.
+ */
+int sdattn_linear(const void *x, const void *w, const void *bias, void *y, int B, int L, int K,
+                  int N, int H, sdattn_layout x_layout, sdattn_layout y_layout, sdattn_dtype dtype,
+                  void *stream);
+
+/*
+ * SD's attention block around Eq. 3 (multi-head attention of latent tokens x
+ * over context tokens ctx; ctx = x for self-attention):
+ *   Q = x wq^T, K = ctx wk^T, V = ctx wv^T, split into H heads of D = C/H;
+ *   O_h = softmax(scale Q_h K_h^T) V_h;  out = [O_0 | ... | O_{H-1}] wo^T + bo
+ *
+ *   x [B, Lq, C], ctx [B, Lk, Cc], out [B, Lq, C]; wq, wo [C, C]; wk, wv [C, Cc];
+ *   bo [C] or NULL; all of `dtype`.
+ *   workspace: device memory of at least sdattn_attention_block_workspace(B, Lq, Lk, C)
+ *   bytes, 16-byte aligned, owned by the caller; it receives Q, K, V and O.
+ *
+ * Five launches on `stream`: three sdattn_linear (heads layout out), the
+ * attention forward, and sdattn_linear (heads layout in).  Requirements: those
+ * of the five calls; D % 8 == 0, D <= 256; no argument may overlap out or the
+ * workspace.
+ */
+long long sdattn_attention_block_workspace(int B, int Lq, int Lk, int C);
+int sdattn_attention_block(const void *x, const void *ctx, const void *wq, const void *wk,
+                           const void *wv, const void *wo, const void *bo, void *out,
+                           void *workspace, long long workspace_bytes, int B, int Lq, int Lk,
+                           int C, int Cc, int H, float scale, sdattn_dtype dtype, void *stream);
+
 /* Static English text for a status code (never NULL). */
 const char *sdattn_status_str(int status);
 

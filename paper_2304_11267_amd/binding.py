@@ -27,7 +27,11 @@ DTYPE_F32 = 2
 
 # every symbol include/sdattn.h declares
 EXPORTS = ("sdattn_forward", "sdattn_forward_ex", "sdattn_softmax_rows", "sdattn_logits",
-           "sdattn_softmax_pv", "sdattn_status_str", "sdattn_last_hip_error", "sdattn_version")
+           "sdattn_softmax_pv", "sdattn_linear", "sdattn_attention_block_workspace",
+           "sdattn_attention_block", "sdattn_status_str", "sdattn_last_hip_error", "sdattn_version")
+
+LAYOUT_ROWS = 0
+LAYOUT_HEADS = 1
 
 _lib = None
 
@@ -64,6 +68,13 @@ def load_library():
     lib.sdattn_logits.restype = i32
     lib.sdattn_softmax_pv.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, vp]
     lib.sdattn_softmax_pv.restype = i32
+    lib.sdattn_linear.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, i32, vp]
+    lib.sdattn_linear.restype = i32
+    lib.sdattn_attention_block_workspace.argtypes = [i32, i32, i32, i32]
+    lib.sdattn_attention_block_workspace.restype = i64
+    lib.sdattn_attention_block.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i64, i32, i32, i32,
+                                           i32, i32, i32, f32, i32, vp]
+    lib.sdattn_attention_block.restype = i32
     lib.sdattn_status_str.argtypes = [i32]
     lib.sdattn_status_str.restype = ctypes.c_char_p
     lib.sdattn_last_hip_error.argtypes = []
@@ -107,10 +118,23 @@ def _dev(t, name):
     return ctypes.c_void_p(t.data_ptr())
 
 
+def _expect(t, shape, like, name):
+    """Raise unless tensor t has exactly `shape` and the element type of `like`:
+    the C entry points see only pointers and sizes, so a tensor smaller than
+    the sizes say would be read or written past its end."""
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if like is not None and t.dtype != like.dtype:
+        raise TypeError(f"{name} is {t.dtype}, expected {like.dtype}")
+
+
 def forward(q, k, v, out, scale: float, stream=None):
     """out = softmax(scale * q k^T) v for q/out [B,H,Lq,D], k/v [B,H,Lk,D], fp16."""
     B, H, Lq, D = q.shape
     Lk = k.shape[2]
+    _expect(k, (B, H, Lk, D), q, "k")
+    _expect(v, (B, H, Lk, D), q, "v")
+    _expect(out, q.shape, q, "out")
     status = load_library().sdattn_forward(
         _dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(out, "out"),
         B, H, Lq, Lk, D, ctypes.c_float(scale), _stream(stream))
@@ -122,6 +146,13 @@ def forward_ex(q, k, v, out, scale: float, ls=None, stream=None):
     """forward for fp16 or bf16, optionally writing fp32 (L, S) per row to ls [B,H,Lq,2]."""
     B, H, Lq, D = q.shape
     Lk = k.shape[2]
+    _expect(k, (B, H, Lk, D), q, "k")
+    _expect(v, (B, H, Lk, D), q, "v")
+    _expect(out, q.shape, q, "out")
+    if ls is not None:
+        _expect(ls, (B, H, Lq, 2), None, "ls")
+        if ls.element_size() != 4:
+            raise TypeError("ls must hold float32")
     ls_ptr = _dev(ls, "ls") if ls is not None else None
     status = load_library().sdattn_forward_ex(
         _dev(q, "q"), _dev(k, "k"), _dev(v, "v"), _dev(out, "out"), ls_ptr,
@@ -133,6 +164,10 @@ def forward_ex(q, k, v, out, scale: float, ls=None, stream=None):
 def softmax_rows(a, ls, p=None, scale: float = 1.0, stream=None):
     """Eq. 4 on a [rows, cols]: ls[r] = (L_r, S_r) fp32; p (optional) = exp(scale*a - L)/S."""
     rows, cols = a.shape
+    if ls.numel() != 2 * rows or ls.element_size() != 4:
+        raise ValueError("ls must hold 2 float32 values per row")
+    if p is not None:
+        _expect(p, a.shape, a, "p")
     p_ptr = _dev(p, "p") if p is not None else None
     status = load_library().sdattn_softmax_rows(
         _dev(a, "a"), _dev(ls, "ls"), p_ptr, rows, cols, ctypes.c_float(scale),
@@ -145,6 +180,8 @@ def logits(q, k, a, scale: float, stream=None):
     """a = scale * q k^T: q [B,H,Lq,D], k [B,H,Lk,D] (fp16/bf16), a [B,H,Lq,Lk] (fp16/bf16/fp32)."""
     B, H, Lq, D = q.shape
     Lk = k.shape[2]
+    _expect(k, (B, H, Lk, D), q, "k")
+    _expect(a, (B, H, Lq, Lk), None, "a")
     status = load_library().sdattn_logits(
         _dev(q, "q"), _dev(k, "k"), _dev(a, "a"), B, H, Lq, Lk, D, ctypes.c_float(scale),
         _dtype_code(q), _dtype_code(a), _stream(stream))
@@ -156,8 +193,64 @@ def softmax_pv(a, ls, v, out, stream=None):
     """out = exp(a - L) / S times v, with (L, S) = ls [B,H,Lq,2] fp32 of a's rows."""
     B, H, Lq, Lk = a.shape
     D = v.shape[3]
+    _expect(v, (B, H, Lk, D), None, "v")
+    _expect(out, (B, H, Lq, D), v, "out")
+    if ls.numel() != 2 * B * H * Lq or ls.element_size() != 4:
+        raise ValueError("ls must hold 2 float32 values per row")
     status = load_library().sdattn_softmax_pv(
         _dev(a, "a"), _dev(ls, "ls"), _dev(v, "v"), _dev(out, "out"), B, H, Lq, Lk, D,
         _dtype_code(a), _dtype_code(v), _stream(stream))
     _check("sdattn_softmax_pv", status)
+    return out
+
+
+def linear(x, w, y, bias=None, heads=1, x_layout=LAYOUT_ROWS, y_layout=LAYOUT_ROWS, stream=None):
+    """y = x w^T + bias over token rows.  Rows layout tensors are [B, L, C], heads layout
+    [B, H, L, C/H]; w is [N, K] (out, in)."""
+    if x_layout == LAYOUT_HEADS:
+        B, H, L, hw = x.shape
+        K = H * hw
+    else:
+        B, L, K = x.shape
+    N = w.shape[0]
+    _expect(w, (N, K), x, "w")
+    if bias is not None:
+        _expect(bias, (N,), x, "bias")
+    if y_layout == LAYOUT_HEADS:
+        if heads < 1 or N % heads:
+            raise ValueError("heads must divide the output channels")
+        _expect(y, (B, heads, L, N // heads), x, "y")
+    else:
+        _expect(y, (B, L, N), x, "y")
+    if x_layout == LAYOUT_HEADS and H != heads:
+        raise ValueError("x's head count differs from heads")
+    status = load_library().sdattn_linear(
+        _dev(x, "x"), _dev(w, "w"), _dev(bias, "bias") if bias is not None else None, _dev(y, "y"),
+        B, L, K, N, heads, x_layout, y_layout, _dtype_code(x), _stream(stream))
+    _check("sdattn_linear", status)
+    return y
+
+
+def attention_block_workspace(B, Lq, Lk, C):
+    """Bytes of workspace sdattn_attention_block needs."""
+    return int(load_library().sdattn_attention_block_workspace(B, Lq, Lk, C))
+
+
+def attention_block(x, ctx, wq, wk, wv, wo, bo, out, workspace, heads, scale, stream=None):
+    """SD's attention block: out = MHA(x, ctx) with weights [out, in]; workspace is a device
+    tensor of at least attention_block_workspace(...) bytes."""
+    B, Lq, C = x.shape
+    Lk, Cc = ctx.shape[1], ctx.shape[2]
+    _expect(ctx, (B, Lk, Cc), x, "ctx")
+    for t, shape, name in ((wq, (C, C), "wq"), (wk, (C, Cc), "wk"), (wv, (C, Cc), "wv"),
+                           (wo, (C, C), "wo"), (out, (B, Lq, C), "out")):
+        _expect(t, shape, x, name)
+    if bo is not None:
+        _expect(bo, (C,), x, "bo")
+    status = load_library().sdattn_attention_block(
+        _dev(x, "x"), _dev(ctx, "ctx"), _dev(wq, "wq"), _dev(wk, "wk"), _dev(wv, "wv"),
+        _dev(wo, "wo"), _dev(bo, "bo") if bo is not None else None, _dev(out, "out"),
+        _dev(workspace, "workspace"), workspace.numel() * workspace.element_size(),
+        B, Lq, Lk, C, Cc, heads, ctypes.c_float(scale), _dtype_code(x), _stream(stream))
+    _check("sdattn_attention_block", status)
     return out

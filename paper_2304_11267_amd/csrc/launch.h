@@ -65,4 +65,18 @@ struct SoftmaxPvArgs {
 };
 hipError_t launch_softmax_pv(const SoftmaxPvArgs& a);
 
+// The projections around the attention (linear.hip).
+struct LinearArgs {
+    const void* x;
+    const void* w;      // [N, K]
+    const void* bias;   // [N] or null
+    void* y;
+    int B, L, K, N, H;
+    bool x_heads, y_heads;   // [B, H, L, C/H] instead of [B, L, C]
+    int dtype;
+    void* stream;
+};
+long long linear_grid(int B, int L, int N);
+hipError_t launch_linear(const LinearArgs& a);
+
 }  // namespace sdattn

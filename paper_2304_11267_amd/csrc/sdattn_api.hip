@@ -105,6 +105,39 @@ int check_twopass(int B, int H, int Lq, int Lk, int D, int dtype, int a_dtype, l
     return SDATTN_OK;
 }
 
+// Checks of sdattn_linear; fills the launch arguments.
+int check_linear(const void* x, const void* w, const void* bias, void* y, int B, int L, int K,
+                 int N, int H, int x_layout, int y_layout, int dtype, void* stream,
+                 sdattn::LinearArgs* args) {
+    if (!x || !w || !y) return SDATTN_ERR_INVALID_ARG;
+    if (B < 1 || L < 1 || K < 1 || N < 1) return SDATTN_ERR_INVALID_ARG;
+    if ((x_layout != SDATTN_ROWS && x_layout != SDATTN_HEADS) ||
+        (y_layout != SDATTN_ROWS && y_layout != SDATTN_HEADS))
+        return SDATTN_ERR_INVALID_ARG;
+    if (dtype != SDATTN_F16 && dtype != SDATTN_BF16) {
+        return dtype == SDATTN_F32 ? SDATTN_ERR_UNSUPPORTED : SDATTN_ERR_INVALID_ARG;
+    }
+    const bool xh = x_layout == SDATTN_HEADS, yh = y_layout == SDATTN_HEADS;
+    if ((xh || yh) && H < 1) return SDATTN_ERR_INVALID_ARG;
+    if (K % 8 != 0 || N % 8 != 0) return SDATTN_ERR_UNSUPPORTED;
+    if (xh && (K % H != 0 || (K / H) % 8 != 0)) return SDATTN_ERR_UNSUPPORTED;
+    if (yh && (N % H != 0 || (N / H) % 8 != 0)) return SDATTN_ERR_UNSUPPORTED;
+    const long long nx = checked_mul({B, L, K}), ny = checked_mul({B, L, N}), nw = checked_mul({N, K});
+    if (nx < 0 || ny < 0 || nw < 0 || (long long)B * L > INT_MAX / 2) return SDATTN_ERR_UNSUPPORTED;
+    if (sdattn::linear_grid(B, L, N) > INT_MAX) return SDATTN_ERR_UNSUPPORTED;
+    if (!aligned(x, 16) || !aligned(w, 16) || !aligned(y, 16) || (bias && !aligned(bias, 2)))
+        return SDATTN_ERR_MISALIGNED;
+    const unsigned long long yb = 2ULL * ny;
+    if (overlap(y, yb, x, 2ULL * nx) || overlap(y, yb, w, 2ULL * nw) ||
+        (bias && overlap(y, yb, bias, 2ULL * N)))
+        return SDATTN_ERR_INVALID_ARG;
+    *args = sdattn::LinearArgs{x, w, bias, y, B, L, K, N, xh || yh ? H : 1, xh, yh, dtype, stream};
+    return SDATTN_OK;
+}
+
+// Q, K, V, O in heads layout, each rounded up to 256 bytes
+long long block_part(long long elems) { return (2 * elems + 255) / 256 * 256; }
+
 }  // namespace
 
 extern "C" {
@@ -170,6 +203,75 @@ int sdattn_softmax_pv(const void* a, const float* ls, const void* v, void* out, 
     (void)hipGetLastError();
     sdattn::SoftmaxPvArgs args{a, ls, v, out, B, H, Lq, Lk, D, (int)dtype, (int)a_dtype, stream};
     return finish(sdattn::launch_softmax_pv(args));
+}
+
+int sdattn_linear(const void* x, const void* w, const void* bias, void* y, int B, int L, int K,
+                  int N, int H, sdattn_layout x_layout, sdattn_layout y_layout, sdattn_dtype dtype,
+                  void* stream) {
+    sdattn::LinearArgs args;
+    const int st = check_linear(x, w, bias, y, B, L, K, N, H, (int)x_layout, (int)y_layout,
+                                (int)dtype, stream, &args);
+    if (st != SDATTN_OK) return st;
+    (void)hipGetLastError();
+    return finish(sdattn::launch_linear(args));
+}
+
+long long sdattn_attention_block_workspace(int B, int Lq, int Lk, int C) {
+    const long long nq = checked_mul({B, Lq, C}), nk = checked_mul({B, Lk, C});
+    if (nq < 0 || nk < 0) return -1;
+    return 2 * block_part(nq) + 2 * block_part(nk);
+}
+
+int sdattn_attention_block(const void* x, const void* ctx, const void* wq, const void* wk,
+                           const void* wv, const void* wo, const void* bo, void* out,
+                           void* workspace, long long workspace_bytes, int B, int Lq, int Lk,
+                           int C, int Cc, int H, float scale, sdattn_dtype dtype, void* stream) {
+    if (!x || !ctx || !wq || !wk || !wv || !wo || !out || !workspace) return SDATTN_ERR_INVALID_ARG;
+    if (B < 1 || Lq < 1 || Lk < 1 || C < 1 || Cc < 1 || H < 1) return SDATTN_ERR_INVALID_ARG;
+    if (C % H != 0) return SDATTN_ERR_INVALID_ARG;
+    const long long need = sdattn_attention_block_workspace(B, Lq, Lk, C);
+    if (need < 0) return SDATTN_ERR_UNSUPPORTED;
+    if (workspace_bytes < need) return SDATTN_ERR_INVALID_ARG;
+    if (!aligned(workspace, 16)) return SDATTN_ERR_MISALIGNED;
+    const int D = C / H;
+    char* ws = (char*)workspace;
+    void* q = ws;
+    void* k = ws + block_part((long long)B * Lq * C);
+    void* v = (char*)k + block_part((long long)B * Lk * C);
+    void* o = (char*)v + block_part((long long)B * Lk * C);
+    // the inputs and the output must stay clear of the workspace and of each other
+    const unsigned long long ob = 2ULL * B * Lq * C;
+    const void* ins[] = {x, ctx, wq, wk, wv, wo, bo};
+    const unsigned long long insz[] = {2ULL * B * Lq * C, 2ULL * B * Lk * Cc, 2ULL * C * C,
+                                       2ULL * C * Cc, 2ULL * C * Cc, 2ULL * C * C, 2ULL * C};
+    for (int i = 0; i < 7; ++i) {
+        if (!ins[i]) continue;
+        if (overlap(ins[i], insz[i], workspace, (unsigned long long)need) ||
+            overlap(ins[i], insz[i], out, ob))
+            return SDATTN_ERR_INVALID_ARG;
+    }
+    if (overlap(out, ob, workspace, (unsigned long long)need)) return SDATTN_ERR_INVALID_ARG;
+    sdattn::LinearArgs pq, pk, pv, po;
+    int st;
+    if ((st = check_linear(x, wq, nullptr, q, B, Lq, C, C, H, SDATTN_ROWS, SDATTN_HEADS, (int)dtype,
+                           stream, &pq)) != SDATTN_OK ||
+        (st = check_linear(ctx, wk, nullptr, k, B, Lk, Cc, C, H, SDATTN_ROWS, SDATTN_HEADS,
+                           (int)dtype, stream, &pk)) != SDATTN_OK ||
+        (st = check_linear(ctx, wv, nullptr, v, B, Lk, Cc, C, H, SDATTN_ROWS, SDATTN_HEADS,
+                           (int)dtype, stream, &pv)) != SDATTN_OK ||
+        (st = check_linear(o, wo, bo, out, B, Lq, C, C, H, SDATTN_HEADS, SDATTN_ROWS, (int)dtype,
+                           stream, &po)) != SDATTN_OK)
+        return st;
+    if ((st = check_attention(q, k, v, o, nullptr, B, H, Lq, Lk, D, scale, (int)dtype)) != SDATTN_OK)
+        return st;
+    (void)hipGetLastError();
+    hipError_t e;
+    if ((e = sdattn::launch_linear(pq)) != hipSuccess) return finish(e);
+    if ((e = sdattn::launch_linear(pk)) != hipSuccess) return finish(e);
+    if ((e = sdattn::launch_linear(pv)) != hipSuccess) return finish(e);
+    sdattn::AttnArgs aa{q, k, v, o, nullptr, B, H, Lq, Lk, D, scale, (int)dtype, stream};
+    if ((e = sdattn::launch_attn_fwd(aa)) != hipSuccess) return finish(e);
+    return finish(sdattn::launch_linear(po));
 }
 
 const char* sdattn_status_str(int status) {

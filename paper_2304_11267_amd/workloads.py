@@ -146,3 +146,73 @@ def sample_rows(B, H, Lq, per_head, seed):
         pick.update({0, Lq - 1})
         out.extend(bh * Lq + i for i in sorted(pick))
     return np.asarray(out, dtype=np.int64)
+
+
+# SD1.4's attention blocks around Eq. 3: channels C = H * D per level, the
+# text context of CLIP ViT-L/14 (77 tokens x 768 channels) for cross-attention.
+CONTEXT_CHANNELS = 768
+
+
+@dataclass(frozen=True)
+class BlockCase:
+    name: str
+    B: int
+    Lq: int
+    Lk: int
+    C: int          # latent channels (H heads of D)
+    Cc: int         # context channels (C for self-attention)
+    H: int
+    seed: int
+    self_attn: bool
+
+    @property
+    def D(self) -> int:
+        return self.C // self.H
+
+    @property
+    def scale(self) -> float:
+        return float(np.float32(1.0 / np.sqrt(self.D)))
+
+    @property
+    def flops(self) -> int:
+        """Algorithmic flops: four projections (2 per multiply-add) and Eq. 3."""
+        proj = 2 * self.B * (self.Lq * self.C * self.C * 2 + self.Lk * self.Cc * self.C * 2)
+        return proj + 4 * self.B * self.H * self.Lq * self.Lk * self.D
+
+
+def _block(name, level, self_attn, seed):
+    L, D = LEVELS[level]
+    C = HEADS * D
+    return BlockCase(name, BATCH, L, L if self_attn else TEXT_TOKENS, C,
+                     C if self_attn else CONTEXT_CHANNELS, HEADS, seed, self_attn)
+
+
+BLOCK_CASES = {
+    "blk64_self": _block("blk64_self", 64, True, SEED0 + 21),
+    "blk64_cross": _block("blk64_cross", 64, False, SEED0 + 22),
+    "blk32_self": _block("blk32_self", 32, True, SEED0 + 23),
+    "blk16_cross": _block("blk16_cross", 16, False, SEED0 + 24),
+}
+
+
+def make_block(B, Lq, Lk, C, Cc, seed, self_attn=False, dtype="f16"):
+    """Draw x [B,Lq,C], ctx [B,Lk,Cc] (x itself for self-attention), then wq, wk,
+    wv, wo (weights [out, in]) and bo, in that order, from default_rng(seed) in
+    float32: tokens ~ N(0, 1), weights ~ N(0, 1/fan_in), bias ~ N(0, 0.01).
+    Returns (x, ctx, wq, wk, wv, wo, bo) as float16 (or bf16 bit patterns)."""
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((B, Lq, C), dtype=np.float32)
+    ctx = x if self_attn else rng.standard_normal((B, Lk, Cc), dtype=np.float32)
+    ws = [rng.standard_normal((C, fan), dtype=np.float32) / np.float32(np.sqrt(fan))
+          for fan in (C, Cc, Cc, C)]
+    bo = rng.standard_normal(C, dtype=np.float32) * np.float32(0.1)
+    out = [x, ctx, *ws, bo]
+    if dtype == "f16":
+        return tuple(t.astype(np.float16) for t in out)
+    if dtype == "bf16":
+        return tuple(to_bf16_bits(t) for t in out)
+    raise ValueError(f"unknown dtype {dtype!r}")
+
+
+def block_inputs(case: BlockCase, dtype="f16"):
+    return make_block(case.B, case.Lq, case.Lk, case.C, case.Cc, case.seed, case.self_attn, dtype)

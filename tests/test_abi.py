@@ -178,3 +178,51 @@ def test_softmax_pv_checks(lib):
     assert pv(lib, v=ctypes.c_void_p(0x30000008)) == MISALIGNED
     assert pv(lib, o=ctypes.c_void_p(0x10000000 + 1024)) == INVALID      # out inside a
     assert pv(lib, o=ctypes.c_void_p(0x50000000 - 64)) == INVALID        # out's tail runs into ls
+
+
+ROWS, HEADS_L = 0, 1
+
+
+def lin(lib, x=QA, w=KA, b=None, y=OA, B=2, L=64, K=320, N=320, H=8, xl=ROWS, yl=HEADS_L, dtype=F16):
+    return lib.sdattn_linear(x, w, b, y, B, L, K, N, H, xl, yl, dtype, None)
+
+
+def test_linear_checks(lib):
+    for field in ("x", "w", "y"):
+        assert lin(lib, **{field: None}) == INVALID
+    for field in ("B", "L", "K", "N"):
+        assert lin(lib, **{field: 0}) == INVALID
+    assert lin(lib, H=0) == INVALID
+    assert lin(lib, xl=2) == INVALID
+    assert lin(lib, dtype=F32) == UNSUPPORTED
+    assert lin(lib, K=324) == UNSUPPORTED               # K % 8
+    assert lin(lib, N=320, H=3) == UNSUPPORTED          # heads do not divide N
+    assert lin(lib, N=96, H=8) == UNSUPPORTED           # head width 12 % 8
+    assert lin(lib, y=ctypes.c_void_p(0x40000000 + 4)) == MISALIGNED
+    assert lin(lib, y=ctypes.c_void_p(0x10000000 + 1024)) == INVALID   # y inside x
+    assert lin(lib, b=ctypes.c_void_p(0x40000000 + 64)) == INVALID    # bias inside y
+
+
+def blk(lib, ws=ctypes.c_void_p(0x60000000), wsb=1 << 26, **kw):
+    a = dict(x=QA, ctx=KA, wq=ctypes.c_void_p(0x70000000), wk=ctypes.c_void_p(0x71000000),
+             wv=ctypes.c_void_p(0x72000000), wo=ctypes.c_void_p(0x73000000),
+             bo=ctypes.c_void_p(0x74000000), out=OA, B=2, Lq=64, Lk=77, C=320, Cc=768, H=8,
+             scale=0.158, dtype=F16)
+    a.update(kw)
+    return lib.sdattn_attention_block(a["x"], a["ctx"], a["wq"], a["wk"], a["wv"], a["wo"], a["bo"],
+                                      a["out"], ws, wsb, a["B"], a["Lq"], a["Lk"], a["C"], a["Cc"],
+                                      a["H"], ctypes.c_float(a["scale"]), a["dtype"], None)
+
+
+def test_attention_block_checks(lib):
+    need = lib.sdattn_attention_block_workspace(2, 64, 77, 320)
+    assert need >= 2 * 2 * (2 * 64 * 320 + 2 * 77 * 320)
+    assert blk(lib, wsb=need - 1) == INVALID
+    assert blk(lib, ws=None) == INVALID
+    assert blk(lib, ws=ctypes.c_void_p(0x60000008)) == MISALIGNED
+    assert blk(lib, C=321, H=8) == INVALID              # heads do not divide C
+    assert blk(lib, C=96, H=8) == UNSUPPORTED           # head width 12
+    assert blk(lib, Cc=770) == UNSUPPORTED              # context channels % 8
+    assert blk(lib, scale=float("inf")) == INVALID
+    assert blk(lib, out=ctypes.c_void_p(0x60000000 + 4096)) == INVALID   # out inside the workspace
+    assert blk(lib, x=ctypes.c_void_p(0x60000000 + 1024)) == INVALID     # x inside the workspace

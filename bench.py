@@ -157,6 +157,8 @@ def main():
         out["cross"].update(cold_cross(torch, sd, wl, dev, stream, cross_case))
         out["softmax_rows"] = bench_softmax_rows(torch, sd, dev, stream)
         out["two_pass"] = bench_two_pass(torch, sd, stream, self_case, (sq, sk, sv), self_ms)
+        out["attention_block"] = bench_block(torch, sd, wl, dev, stream,
+                                             {"self": self_ms, "cross": warm_ms})
 
     if args.copy_calibration:
         out["copy_calibration"] = copy_calibration(torch, dev, stream)
@@ -266,6 +268,39 @@ def bench_softmax_rows(torch, sd, dev, stream, reps=10):
         res[name] = {"avg_kernel_us": round(ms * 1e3, 2), "bytes": nbytes, "gbs": round(gbs, 1),
                      "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)}
     res["shape"] = f"{rows}x{cols} fp16 (A = Q K^T of the 64x64 level; A is L2/MALL-cold at 537 MB)"
+    return res
+
+
+def bench_block(torch, sd, wl, dev, stream, attn_ms, launches=50, reps=3):
+    """SD's attention block at the 64x64 level (Q/K/V projections, the fused
+    attention, the output projection with bias), self and cross, launched back
+    to back behind a busy GPU; weights N(0, 1/fan_in) standing in for trained ones."""
+    res = {}
+    for kind in ("self", "cross"):
+        case = wl.BLOCK_CASES["blk64_" + kind]
+        x, ctx, wq, wk, wv, wo, bo = (torch.from_numpy(t).to(dev) for t in wl.block_inputs(case))
+        ws = torch.empty(sd.attention_block_workspace(case.B, case.Lq, case.Lk, case.C),
+                         dtype=torch.uint8, device=dev)
+        out = torch.empty_like(x)
+        call = lambda: sd.attention_block(x, ctx, wq, wk, wv, wo, bo, out, ws, case.H, case.scale, stream)
+        call()
+        torch.cuda.synchronize()
+        best = None
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda._sleep(20_000_000)
+            e0.record(stream)
+            for _ in range(launches):
+                call()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / launches
+            best = ms if best is None else min(best, ms)
+        res[kind] = {"us": round(best * 1e3, 2), "flops": case.flops,
+                     "tflops": round(case.flops / (best * 1e-3) / 1e12, 1),
+                     "attention_us": round(attn_ms[kind] * 1e3, 2),
+                     "projections_us": round((best - attn_ms[kind]) * 1e3, 2),
+                     "shape": f"x [{case.B},{case.Lq},{case.C}] ctx [{case.B},{case.Lk},{case.Cc}] H{case.H}"}
     return res
 
 

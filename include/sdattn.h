@@ -161,8 +161,8 @@ typedef enum {
  *         and rounded to nearest even
  *   H     heads of a SDATTN_HEADS side (ignored when neither side uses it)
  *
- * Requirements: x, w, y 16-byte aligned; B, L, K, N >= 1; K % 8 == 0 and
- * N % 8 == 0; on a SDATTN_HEADS side H >= 1 divides that side's channels into
+ * Requirements: x, w, y 16-byte aligned, bias 8-byte aligned; B, L, K, N >= 1;
+ * K and N multiples of 8, at most 65536; on a SDATTN_HEADS side H >= 1 divides that side's channels into
  * widths that are multiples of 8; y must not overlap x, w or bias.
  */
 int sdattn_linear(const void *x, const void *w, const void *bias, void *y, int B, int L, int K,
@@ -180,10 +180,11 @@ int sdattn_linear(const void *x, const void *w, const void *bias, void *y, int B
  *   workspace: device memory of at least sdattn_attention_block_workspace(B, Lq, Lk, C)
  *   bytes, 16-byte aligned, owned by the caller; it receives Q, K, V and O.
  *
- * Five launches on `stream`: three sdattn_linear (heads layout out), the
- * attention forward, and sdattn_linear (heads layout in).  Requirements: those
- * of the five calls; D % 8 == 0, D <= 256; no argument may overlap out or the
- * workspace.
+ * Three launches on `stream`: the Q, K and V projections together (heads
+ * layout out), the attention forward, and the output projection (heads layout
+ * in).  Requirements: those of sdattn_linear for each projection and of
+ * sdattn_forward_ex for the attention (D % 8 == 0, D <= 256); no argument may
+ * overlap out or the workspace.
  */
 long long sdattn_attention_block_workspace(int B, int Lq, int Lk, int C);
 int sdattn_attention_block(const void *x, const void *ctx, const void *wq, const void *wk,

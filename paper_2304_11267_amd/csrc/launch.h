@@ -78,5 +78,9 @@ struct LinearArgs {
 };
 long long linear_grid(int B, int L, int N);
 hipError_t launch_linear(const LinearArgs& a);
+// Up to kMaxLinearProblems products of one element type and one pair of
+// layouts in a single launch (e.g. the Q, K and V projections).
+constexpr int kMaxLinearProblems = 3;
+hipError_t launch_linear_group(const LinearArgs* a, int n);
 
 }  // namespace sdattn

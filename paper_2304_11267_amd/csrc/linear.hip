@@ -8,11 +8,22 @@
 // head split before Eq. 3; reading O in heads layout is the head merge before
 // the output projection -- neither needs a transpose of its own.
 //
-// The product runs as y^T = w x^T on 32x32x16 MFMAs with one token row per
-// lane (as S^T = K Q^T in the attention kernels): A = 32 weight rows x 16
-// input channels, B = 16 input channels x 32 token rows, both loaded 16 bytes
-// per lane straight from global memory, and each lane ends with 4 consecutive
-// output channels per register group, stored 8 bytes at a time.
+// One launch may carry up to three independent products (the block's Q, K
+// and V projections, whose inputs differ for cross-attention); each
+// workgroup finds its product from its tile index, so the small context
+// projections run beside the large latent one instead of after it.
+//
+// Workgroup tile: 128 token rows x 64 output channels, four waves of 32 rows.
+// Each 64-channel slice of the x and w tiles is copied global -> LDS with
+// global_load_lds (16 bytes per lane, whole 128-byte rows per instruction,
+// no registers), into a ring of kStages slices so that kStages - 1 copies are
+// in flight while one slice is multiplied.  Inside a slice, row r's 16-byte
+// chunk c sits at chunk position c ^ swz(r), which keeps the MFMA operand
+// reads (ds_read_b128, one row per lane) free of bank conflicts.  The product
+// runs as y^T = w x^T on 32x32x16 MFMAs: A = 32 weight rows x 16 channels,
+// B = 16 channels x 32 token rows, one token row per lane; each lane ends with
+// 4 consecutive output channels per register group; the tile goes out through
+// LDS so that each lane stores 16 contiguous bytes.
 #include "device.h"
 #include "launch.h"
 
@@ -20,9 +31,30 @@ namespace sdattn {
 
 namespace {
 
-constexpr int kLinM = 128;   // token rows per workgroup (4 waves x 32)
-constexpr int kLinN = 64;    // output channels per workgroup (2 MFMA tiles)
-constexpr int kLinK = 64;    // input channels per loop step (4 MFMA k-steps)
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+constexpr int kBM = 128;                          // token rows per workgroup
+constexpr int kBN = 64;                           // output channels per workgroup
+constexpr int kBK = 64;                           // input channels per slice
+constexpr int kUnits = (kBM + kBN) * kBK / 8;     // 16-byte chunks per slice (1536)
+constexpr int kSliceBytes = kUnits * 16;          // 24 KiB
+constexpr int kCopies = kUnits / 64 / 4;          // copy instructions per wave per slice (6)
+constexpr int kStages = 3;
+constexpr int kLdsBytes = kStages * kSliceBytes;  // 72 KiB: two workgroups per CU
+
+struct LinProblem {
+    const uint16_t* x;
+    const uint16_t* w;
+    const uint16_t* bias;   // null: no bias
+    uint16_t* y;
+    int M, K, N, L;         // M = B*L token rows
+    int xhw, yhw;           // head widths of the heads layouts (1 for rows layout)
+    int nnt, tile0;         // channel tiles; first tile index of this product
+};
+struct LinGroup {
+    LinProblem p[kMaxLinearProblems];
+    int n;
+};
 
 __device__ __forceinline__ int xcd_remap(int bid, int nblk) {
     const int per = nblk / 8, rem = nblk % 8;
@@ -30,53 +62,141 @@ __device__ __forceinline__ int xcd_remap(int bid, int nblk) {
     return xcd < rem ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
 }
 
-// Element offset of channel c of token row m = b*L + l in a tensor of C channels.
+// chunk-position swizzle of row r: distinct for any 8 consecutive rows, and
+// (r & 1, swz) distinct for any 16 consecutive rows
+__device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
+// c / hw for 0 <= c < 2^16 and 8 <= hw: the fp32 quotient is within one of
+// the true one, and one correction step makes it exact.
+__device__ __forceinline__ int div_small(int c, int hw, float inv_hw) {
+    int h = (int)((float)c * inv_hw);
+    h -= (h * hw > c) ? 1 : 0;
+    h += ((h + 1) * hw <= c) ? 1 : 0;
+    return h;
+}
+
+// Element offset of token row m = b*L + l (channel 0, head 0) in a tensor of
+// C channels, and of channel c relative to it.
 template <bool HEADS>
-__device__ __forceinline__ size_t row_offset(int m, int c, int L, int C, int hw) {
+__device__ __forceinline__ size_t row_base(int m, int L, int C, int hw) {
     if constexpr (HEADS) {
         const int b = m / L, l = m - b * L;
-        const int h = c / hw, d = c - h * hw;
-        return ((size_t)(b * (C / hw) + h) * L + l) * hw + d;
+        return ((size_t)b * (C / hw) * L + l) * hw;
     } else {
-        return (size_t)m * C + c;
+        return (size_t)m * C;
+    }
+}
+template <bool HEADS>
+__device__ __forceinline__ size_t chan_offset(int c, int L, int hw, float inv_hw) {
+    if constexpr (HEADS) {
+        const int h = div_small(c, hw, inv_hw);
+        return (size_t)h * L * hw + (c - h * hw);
+    } else {
+        return (size_t)c;
     }
 }
 
-template <int ET, bool XH, bool YH, bool BIAS>
-__global__ __launch_bounds__(256) void linear_kernel(const uint16_t* __restrict__ X,
-                                                     const uint16_t* __restrict__ W,
-                                                     const uint16_t* __restrict__ Bias,
-                                                     uint16_t* __restrict__ Y, int M, int K, int N,
-                                                     int L, int xhw, int yhw, int nmt, int nnt) {
-    const int tid = threadIdx.x;
+// Wait until at most `ahead` slices of this wave's copies are still in flight.
+__device__ __forceinline__ void wait_slices(int ahead) {
+    static_assert(kStages == 3, "wait_slices covers ahead = 0 and 1");
+    if (ahead >= 1) __builtin_amdgcn_s_waitcnt(vm_wait(kCopies));
+    else __builtin_amdgcn_s_waitcnt(vm_wait(0));
+}
+
+// Workgroup barrier after this wave's LDS reads have returned.  The slice
+// copies are waited for explicitly (wait_slices); a fence here would drain
+// every copy still in flight, since they count as LDS writes.  The memory
+// clobber keeps the compiler from moving LDS reads across the barrier.
+__device__ __forceinline__ void lds_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+template <int ET, bool XH, bool YH>
+__global__ __launch_bounds__(256) void linear_kernel(const LinGroup grp) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
     const int lane = lane_id();
     const int l32 = lane & 31;
     const int half = lane >> 5;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 
     const int tile = xcd_remap(blockIdx.x, gridDim.x);
-    const int nt = tile % nnt;          // consecutive workgroups share the token rows
-    const int mt = tile / nnt;
-    const int m = mt * kLinM + wave * 32 + l32;      // this lane's token row
-    const int n0 = nt * kLinN;
-    const bool mvalid = m < M;
-    const int ms = mvalid ? m : 0;
+    const int pi = (grp.n > 2 && tile >= grp.p[2].tile0) ? 2 : (grp.n > 1 && tile >= grp.p[1].tile0) ? 1 : 0;
+    const LinProblem& P = grp.p[pi];
+    const uint16_t* __restrict__ X = P.x;
+    const uint16_t* __restrict__ W = P.w;
+    const int M = P.M, K = P.K, N = P.N, L = P.L, xhw = P.xhw;
+    const int local = tile - P.tile0;
+    const int nt = local % P.nnt;        // consecutive workgroups share the token rows
+    const int m0 = (local / P.nnt) * kBM;
+    const int n0 = nt * kBN;
+    const int nk = (K + kBK - 1) / kBK;
 
-    // operands of one 16-channel k-step at input channel k: x[m][k + 8*half ..]
-    // and w[n0 + 32t + l32][k + 8*half ..]; zero past K, N or M
-    auto load_x = [&](int k) __attribute__((always_inline)) -> u32x4 {
-        const int c = k + 8 * half;
-        u32x4 v = {0u, 0u, 0u, 0u};
-        if (c < K && mvalid) v = *(const u32x4*)(X + row_offset<XH>(ms, c, L, K, xhw));
-        return v;
+    // Copy j of this wave moves 16-byte chunk c of tile row r (x rows first,
+    // then w rows); rows past M or N repeat the last row (their outputs are
+    // never stored), channels past K repeat the last chunk (their operands are
+    // zeroed before use).  Row bases are fixed across slices.
+    size_t cbase[kCopies];
+    int cch[kCopies];
+#pragma unroll
+    for (int j = 0; j < kCopies; ++j) {
+        const int u0 = (wave * kCopies + j) * 64;
+        const int u = u0 + lane;
+        if (u0 < kBM * 8) {
+            const int r = u >> 3;
+            cch[j] = 8 * ((u & 7) ^ swz(r));
+            cbase[j] = row_base<XH>(min(m0 + r, M - 1), L, K, xhw);
+        } else {
+            const int r = (u >> 3) - kBM;
+            cch[j] = 8 * ((u & 7) ^ swz(r));
+            cbase[j] = (size_t)min(n0 + r, N - 1) * K;
+        }
+    }
+    const float inv_xhw = 1.0f / (float)xhw;
+
+    // slice i (channels 64i .. 64i + 63) into ring slot i % kStages
+    auto issue = [&](int i) __attribute__((always_inline)) {
+        const int k0 = i * kBK;
+        char* st = smem + (i % kStages) * kSliceBytes;
+#pragma unroll
+        for (int j = 0; j < kCopies; ++j) {
+            const int u0 = (wave * kCopies + j) * 64;
+            const int ch = min(k0 + cch[j], K - 8);
+            const char* src = u0 < kBM * 8
+                                  ? (const char*)(X + cbase[j] + chan_offset<XH>(ch, L, xhw, inv_xhw))
+                                  : (const char*)(W + cbase[j] + ch);
+            __builtin_amdgcn_global_load_lds(src, (lds_void_t*)(st + u0 * 16), 16, 0, 0);
+        }
     };
-    auto load_w = [&](int k, int t) __attribute__((always_inline)) -> u32x4 {
-        const int c = k + 8 * half;
-        const int n = n0 + 32 * t + l32;
-        u32x4 v = {0u, 0u, 0u, 0u};
-        if (c < K && n < N) v = *(const u32x4*)(W + (size_t)n * K + c);
-        return v;
-    };
+
+    // operand offsets inside a slice: B = x row 32*wave + l32, A_t = w row
+    // 32t + l32, chunk 2s + half for k-step s (rows 32t + l32 share swz(l32))
+    const int hx = swz(l32);
+    int offx[4], offw[2][4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+        const int cpos = (2 * s + half) ^ hx;
+        offx[s] = ((32 * wave + l32) * 8 + cpos) * 16;
+#pragma unroll
+        for (int t = 0; t < 2; ++t) offw[t][s] = ((kBM + 32 * t + l32) * 8 + cpos) * 16;
+    }
+
+    // bias of this lane's output channels (8-byte aligned groups of 4),
+    // fetched before the product
+    const uint16_t* __restrict__ Bias = P.bias;
+    u32x2 bias[2][4];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) bias[t][g] = u32x2{0u, 0u};
+    if (Bias) {
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int n = min(n0 + 32 * t + 8 * g + 4 * half, N - 4);
+                bias[t][g] = *(const u32x2*)(Bias + n);
+            }
+    }
 
     f32x16 acc[2];
 #pragma unroll
@@ -84,93 +204,141 @@ __global__ __launch_bounds__(256) void linear_kernel(const uint16_t* __restrict_
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[t][r] = 0.0f;
 
-    constexpr int S = kLinK / 16;
-    u32x4 xa[S], wa[S][2];
 #pragma unroll
-    for (int s = 0; s < S; ++s) {
-        xa[s] = load_x(16 * s);
-        wa[s][0] = load_w(16 * s, 0);
-        wa[s][1] = load_w(16 * s, 1);
-    }
-    for (int k0 = 0; k0 < K; k0 += kLinK) {
-        u32x4 xb[S], wb[S][2];
-        const bool more = k0 + kLinK < K;
-        if (more) {   // next step's operands while this step's MFMAs run
+    for (int i = 0; i < kStages - 1; ++i)
+        if (i < nk) issue(i);
+
+    for (int i = 0; i < nk; ++i) {
+        wait_slices(min(nk - 1 - i, kStages - 2));
+        lds_barrier();   // slice i is in LDS for every wave; slot (i - 1) % kStages is free
+        if (i + kStages - 1 < nk) issue(i + kStages - 1);
+        const char* st = smem + (i % kStages) * kSliceBytes;
+        const int kval = K - i * kBK;    // channels of this slice inside K (uniform)
+        // all twelve operand reads first, so their latencies overlap
+        u32x4 bf[4], af[2][4];
 #pragma unroll
-            for (int s = 0; s < S; ++s) {
-                xb[s] = load_x(k0 + kLinK + 16 * s);
-                wb[s][0] = load_w(k0 + kLinK + 16 * s, 0);
-                wb[s][1] = load_w(k0 + kLinK + 16 * s, 1);
-            }
+        for (int s = 0; s < 4; ++s) {
+            bf[s] = *(const u32x4*)(st + offx[s]);
+            af[0][s] = *(const u32x4*)(st + offw[0][s]);
+            af[1][s] = *(const u32x4*)(st + offw[1][s]);
+        }
+        if (kval < kBK) {
+#pragma unroll
+            for (int s = 0; s < 4; ++s)
+                if (8 * (2 * s + half) >= kval) {
+                    bf[s] = u32x4{0u, 0u, 0u, 0u};
+                    af[0][s] = bf[s];
+                    af[1][s] = bf[s];
+                }
         }
 #pragma unroll
-        for (int s = 0; s < S; ++s)
-#pragma unroll
-            for (int t = 0; t < 2; ++t) acc[t] = mfma32x32x16<ET>(wa[s][t], xa[s], acc[t]);
-        if (more) {
-#pragma unroll
-            for (int s = 0; s < S; ++s) {
-                xa[s] = xb[s];
-                wa[s][0] = wb[s][0];
-                wa[s][1] = wb[s][1];
-            }
+        for (int s = 0; s < 4; ++s) {
+            acc[0] = mfma32x32x16<ET>(af[0][s], bf[s], acc[0]);
+            acc[1] = mfma32x32x16<ET>(af[1][s], bf[s], acc[1]);
         }
     }
 
-    // output channels n0 + 32t + 8g + 4*half + (0..3) of token row m
-    if (!mvalid) return;
+    // Stage the 128 x 64 output tile (bias added, rounded) in LDS, rows of
+    // kOutStride bytes: lane (l32, half) holds channels 32t + 8g + 4*half + (0..3)
+    // of tile row 32*wave + l32.
+    constexpr int kOutStride = kBN * 2 + 16;
+    static_assert(kBM * kOutStride <= kLdsBytes, "output tile fits in the slice ring");
+    lds_barrier();   // every wave is done with the slices
+    {
+        char* orow = smem + (32 * wave + l32) * kOutStride;
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+        for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-            const int n = n0 + 32 * t + 8 * g + 4 * half;
-            if (n < N) {   // N % 8 == 0: the 4 channels are all inside N and inside one head
+            for (int g = 0; g < 4; ++g) {
                 float v[4];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    v[e] = acc[t][4 * g + e];
-                    if constexpr (BIAS) v[e] += to_float<ET>(Bias[n + e]);
-                }
+                for (int e = 0; e < 4; ++e)
+                    v[e] = acc[t][4 * g + e] +
+                           to_float<ET>((uint16_t)(bias[t][g][e >> 1] >> (16 * (e & 1))));
                 u32x2 w;
                 w[0] = pack2<ET>(v[0], v[1]);
                 w[1] = pack2<ET>(v[2], v[3]);
-                *(u32x2*)(Y + row_offset<YH>(m, n, L, N, yhw)) = w;
+                *(u32x2*)(orow + (32 * t + 8 * g + 4 * half) * 2) = w;
             }
-        }
-}
-
-template <int ET, bool XH, bool YH, bool BIAS>
-hipError_t launch_linear_t(const LinearArgs& a) {
-    const int M = a.B * a.L;
-    const int nmt = (M + kLinM - 1) / kLinM;
-    const int nnt = (a.N + kLinN - 1) / kLinN;
-    const long long nblk = (long long)nmt * nnt;
-    hipLaunchKernelGGL((linear_kernel<ET, XH, YH, BIAS>), dim3((unsigned)nblk), dim3(256), 0,
-                       (hipStream_t)a.stream, (const uint16_t*)a.x, (const uint16_t*)a.w,
-                       (const uint16_t*)a.bias, (uint16_t*)a.y, M, a.K, a.N, a.L,
-                       a.x_heads ? a.K / a.H : 1, a.y_heads ? a.N / a.H : 1, nmt, nnt);
-    return hipGetLastError();
-}
-
-template <int ET>
-hipError_t launch_linear_e(const LinearArgs& a) {
-    const bool b = a.bias != nullptr;
-    if (a.x_heads) {
-        if (a.y_heads) return b ? launch_linear_t<ET, true, true, true>(a) : launch_linear_t<ET, true, true, false>(a);
-        return b ? launch_linear_t<ET, true, false, true>(a) : launch_linear_t<ET, true, false, false>(a);
     }
-    if (a.y_heads) return b ? launch_linear_t<ET, false, true, true>(a) : launch_linear_t<ET, false, true, false>(a);
-    return b ? launch_linear_t<ET, false, false, true>(a) : launch_linear_t<ET, false, false, false>(a);
+    lds_barrier();
+    // 16 bytes per lane: chunk q = tid + 256j is tile row q / 8, channels
+    // 8 (q % 8) .. + 7 (inside one head, as head widths are multiples of 8)
+    uint16_t* __restrict__ Y = P.y;
+    const int yhw = P.yhw;
+    const float inv_yhw = 1.0f / (float)yhw;
+#pragma unroll
+    for (int j = 0; j < kBM * kBN / 8 / 256; ++j) {
+        const int q = (int)threadIdx.x + 256 * j;
+        const int r = q >> 3, c8 = q & 7;
+        const int m = m0 + r, n = n0 + 8 * c8;
+        if (m < M && n < N) {
+            const u32x4 v = *(const u32x4*)(smem + r * kOutStride + c8 * 16);
+            *(u32x4*)(Y + row_base<YH>(m, L, N, yhw) + chan_offset<YH>(n, L, yhw, inv_yhw)) = v;
+        }
+    }
+}
+
+long long tiles_of(const LinearArgs& a) {
+    return ((long long)a.B * a.L + kBM - 1) / kBM * ((a.N + kBN - 1) / kBN);
+}
+
+template <int ET, bool XH, bool YH>
+hipError_t launch_t(const LinGroup& g, long long nblk, void* stream) {
+    static const hipError_t attr = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(&linear_kernel<ET, XH, YH>),
+        hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes);
+    if (attr != hipSuccess) return attr;
+    hipLaunchKernelGGL((linear_kernel<ET, XH, YH>), dim3((unsigned)nblk), dim3(256), kLdsBytes,
+                       (hipStream_t)stream, g);
+    return hipGetLastError();
 }
 
 }  // namespace
 
 long long linear_grid(int B, int L, int N) {
-    return ((long long)B * L + kLinM - 1) / kLinM * ((N + kLinN - 1) / kLinN);
+    LinearArgs a{};
+    a.B = B;
+    a.L = L;
+    a.N = N;
+    return tiles_of(a);
 }
 
-hipError_t launch_linear(const LinearArgs& a) {
-    return a.dtype == kF16 ? launch_linear_e<kF16>(a) : launch_linear_e<kBF16>(a);
+hipError_t launch_linear_group(const LinearArgs* a, int n) {
+    if (n < 1 || n > kMaxLinearProblems) return hipErrorInvalidValue;
+    LinGroup g{};
+    long long nblk = 0;
+    for (int i = 0; i < n; ++i) {
+        if (a[i].dtype != a[0].dtype || a[i].x_heads != a[0].x_heads ||
+            a[i].y_heads != a[0].y_heads || a[i].stream != a[0].stream)
+            return hipErrorInvalidValue;
+        LinProblem& p = g.p[i];
+        p.x = (const uint16_t*)a[i].x;
+        p.w = (const uint16_t*)a[i].w;
+        p.bias = (const uint16_t*)a[i].bias;
+        p.y = (uint16_t*)a[i].y;
+        p.M = a[i].B * a[i].L;
+        p.K = a[i].K;
+        p.N = a[i].N;
+        p.L = a[i].L;
+        p.xhw = a[i].x_heads ? a[i].K / a[i].H : 1;
+        p.yhw = a[i].y_heads ? a[i].N / a[i].H : 1;
+        p.nnt = (a[i].N + kBN - 1) / kBN;
+        p.tile0 = (int)nblk;
+        nblk += tiles_of(a[i]);
+    }
+    g.n = n;
+    if (nblk > 0x7fffffff) return hipErrorInvalidValue;
+    const bool xh = a[0].x_heads, yh = a[0].y_heads;
+    void* s = a[0].stream;
+    if (a[0].dtype == kF16) {
+        if (xh) return yh ? launch_t<kF16, true, true>(g, nblk, s) : launch_t<kF16, true, false>(g, nblk, s);
+        return yh ? launch_t<kF16, false, true>(g, nblk, s) : launch_t<kF16, false, false>(g, nblk, s);
+    }
+    if (xh) return yh ? launch_t<kBF16, true, true>(g, nblk, s) : launch_t<kBF16, true, false>(g, nblk, s);
+    return yh ? launch_t<kBF16, false, true>(g, nblk, s) : launch_t<kBF16, false, false>(g, nblk, s);
 }
+
+hipError_t launch_linear(const LinearArgs& a) { return launch_linear_group(&a, 1); }
 
 }  // namespace sdattn

@@ -119,13 +119,13 @@ int check_linear(const void* x, const void* w, const void* bias, void* y, int B,
     }
     const bool xh = x_layout == SDATTN_HEADS, yh = y_layout == SDATTN_HEADS;
     if ((xh || yh) && H < 1) return SDATTN_ERR_INVALID_ARG;
-    if (K % 8 != 0 || N % 8 != 0) return SDATTN_ERR_UNSUPPORTED;
+    if (K % 8 != 0 || N % 8 != 0 || K > 65536 || N > 65536) return SDATTN_ERR_UNSUPPORTED;
     if (xh && (K % H != 0 || (K / H) % 8 != 0)) return SDATTN_ERR_UNSUPPORTED;
     if (yh && (N % H != 0 || (N / H) % 8 != 0)) return SDATTN_ERR_UNSUPPORTED;
     const long long nx = checked_mul({B, L, K}), ny = checked_mul({B, L, N}), nw = checked_mul({N, K});
     if (nx < 0 || ny < 0 || nw < 0 || (long long)B * L > INT_MAX / 2) return SDATTN_ERR_UNSUPPORTED;
     if (sdattn::linear_grid(B, L, N) > INT_MAX) return SDATTN_ERR_UNSUPPORTED;
-    if (!aligned(x, 16) || !aligned(w, 16) || !aligned(y, 16) || (bias && !aligned(bias, 2)))
+    if (!aligned(x, 16) || !aligned(w, 16) || !aligned(y, 16) || (bias && !aligned(bias, 8)))
         return SDATTN_ERR_MISALIGNED;
     const unsigned long long yb = 2ULL * ny;
     if (overlap(y, yb, x, 2ULL * nx) || overlap(y, yb, w, 2ULL * nw) ||
@@ -266,9 +266,8 @@ int sdattn_attention_block(const void* x, const void* ctx, const void* wq, const
         return st;
     (void)hipGetLastError();
     hipError_t e;
-    if ((e = sdattn::launch_linear(pq)) != hipSuccess) return finish(e);
-    if ((e = sdattn::launch_linear(pk)) != hipSuccess) return finish(e);
-    if ((e = sdattn::launch_linear(pv)) != hipSuccess) return finish(e);
+    const sdattn::LinearArgs qkv[3] = {pq, pk, pv};
+    if ((e = sdattn::launch_linear_group(qkv, 3)) != hipSuccess) return finish(e);
     sdattn::AttnArgs aa{q, k, v, o, nullptr, B, H, Lq, Lk, D, scale, (int)dtype, stream};
     if ((e = sdattn::launch_attn_fwd(aa)) != hipSuccess) return finish(e);
     return finish(sdattn::launch_linear(po));

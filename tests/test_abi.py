@@ -196,6 +196,7 @@ def test_linear_checks(lib):
     assert lin(lib, xl=2) == INVALID
     assert lin(lib, dtype=F32) == UNSUPPORTED
     assert lin(lib, K=324) == UNSUPPORTED               # K % 8
+    assert lin(lib, K=65544) == UNSUPPORTED             # K above 65536
     assert lin(lib, N=320, H=3) == UNSUPPORTED          # heads do not divide N
     assert lin(lib, N=96, H=8) == UNSUPPORTED           # head width 12 % 8
     assert lin(lib, y=ctypes.c_void_p(0x40000000 + 4)) == MISALIGNED

@@ -178,11 +178,12 @@ int sdattn_linear(const void *x, const void *w, const void *bias, void *y, int B
  *   x [B, Lq, C], ctx [B, Lk, Cc], out [B, Lq, C]; wq, wo [C, C]; wk, wv [C, Cc];
  *   bo [C] or NULL; all of `dtype`.
  *   workspace: device memory of at least sdattn_attention_block_workspace(B, Lq, Lk, C)
- *   bytes, 16-byte aligned, owned by the caller; it receives Q, K, V and O.
+ *   bytes, 16-byte aligned, owned by the caller; it receives Q, K, V and O
+ *   (with Lk = 0 the size covers Q and O only, as sdattn_attention_block_kv needs).
  *
  * Three launches on `stream`: the Q, K and V projections together (heads
- * layout out), the attention forward, and the output projection (heads layout
- * in).  Requirements: those of sdattn_linear for each projection and of
+ * layout out), the attention forward (writing O with the heads merged, as
+ * [B, Lq, C]), and the output projection.  Requirements: those of sdattn_linear for each projection and of
  * sdattn_forward_ex for the attention (D % 8 == 0, D <= 256); no argument may
  * overlap out or the workspace.
  */
@@ -191,6 +192,36 @@ int sdattn_attention_block(const void *x, const void *ctx, const void *wq, const
                            const void *wv, const void *wo, const void *bo, void *out,
                            void *workspace, long long workspace_bytes, int B, int Lq, int Lk,
                            int C, int Cc, int H, float scale, sdattn_dtype dtype, void *stream);
+
+/*
+ * The context side of a cross-attention block: K = ctx wk^T and V = ctx wv^T,
+ * written split into H heads (SDATTN_HEADS layout, [B, H, Lk, C/H]).  The text
+ * context is the same at every denoising step (Sec. 3, denoising network), so
+ * a caller computes K and V once per prompt and hands them to
+ * sdattn_attention_block_kv at each step.  One launch on `stream`.
+ *
+ *   ctx [B, Lk, Cc]; wk, wv [C, Cc]; k, v [B, H, Lk, C/H]; all of `dtype`.
+ * Requirements: those of sdattn_linear for both products; k and v must not
+ * overlap each other, ctx or the weights.
+ */
+int sdattn_project_kv(const void *ctx, const void *wk, const void *wv, void *k, void *v, int B,
+                      int Lk, int Cc, int C, int H, sdattn_dtype dtype, void *stream);
+
+/*
+ * sdattn_attention_block with K and V given (from sdattn_project_kv):
+ *   Q = x wq^T split into H heads; O_h = softmax(scale Q_h K_h^T) V_h;
+ *   out = [O_0 | ... | O_{H-1}] wo^T + bo
+ *
+ *   x, out [B, Lq, C]; wq, wo [C, C]; k, v [B, H, Lk, C/H]; bo [C] or NULL.
+ *   workspace: at least sdattn_attention_block_workspace(B, Lq, 0, C) bytes,
+ *   16-byte aligned; it receives Q and O.
+ * Three launches on `stream` (Q projection, attention, output projection);
+ * requirements as for sdattn_attention_block.
+ */
+int sdattn_attention_block_kv(const void *x, const void *wq, const void *k, const void *v,
+                              const void *wo, const void *bo, void *out, void *workspace,
+                              long long workspace_bytes, int B, int Lq, int Lk, int C, int H,
+                              float scale, sdattn_dtype dtype, void *stream);
 
 /* Static English text for a status code (never NULL). */
 const char *sdattn_status_str(int status);

@@ -28,7 +28,8 @@ DTYPE_F32 = 2
 # every symbol include/sdattn.h declares
 EXPORTS = ("sdattn_forward", "sdattn_forward_ex", "sdattn_softmax_rows", "sdattn_logits",
            "sdattn_softmax_pv", "sdattn_linear", "sdattn_attention_block_workspace",
-           "sdattn_attention_block", "sdattn_status_str", "sdattn_last_hip_error", "sdattn_version")
+           "sdattn_attention_block", "sdattn_project_kv", "sdattn_attention_block_kv",
+           "sdattn_status_str", "sdattn_last_hip_error", "sdattn_version")
 
 LAYOUT_ROWS = 0
 LAYOUT_HEADS = 1
@@ -75,6 +76,11 @@ def load_library():
     lib.sdattn_attention_block.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i64, i32, i32, i32,
                                            i32, i32, i32, f32, i32, vp]
     lib.sdattn_attention_block.restype = i32
+    lib.sdattn_project_kv.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp]
+    lib.sdattn_project_kv.restype = i32
+    lib.sdattn_attention_block_kv.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i64, i32, i32, i32,
+                                              i32, i32, f32, i32, vp]
+    lib.sdattn_attention_block_kv.restype = i32
     lib.sdattn_status_str.argtypes = [i32]
     lib.sdattn_status_str.restype = ctypes.c_char_p
     lib.sdattn_last_hip_error.argtypes = []
@@ -253,4 +259,41 @@ def attention_block(x, ctx, wq, wk, wv, wo, bo, out, workspace, heads, scale, st
         _dev(workspace, "workspace"), workspace.numel() * workspace.element_size(),
         B, Lq, Lk, C, Cc, heads, ctypes.c_float(scale), _dtype_code(x), _stream(stream))
     _check("sdattn_attention_block", status)
+    return out
+
+
+def project_kv(ctx, wk, wv, k, v, heads, stream=None):
+    """K = ctx wk^T, V = ctx wv^T split into heads: ctx [B, Lk, Cc], k, v [B, H, Lk, C/H]."""
+    B, Lk, Cc = ctx.shape
+    C = wk.shape[0]
+    _expect(wk, (C, Cc), ctx, "wk")
+    _expect(wv, (C, Cc), ctx, "wv")
+    if heads < 1 or C % heads:
+        raise ValueError("heads must divide the channels")
+    _expect(k, (B, heads, Lk, C // heads), ctx, "k")
+    _expect(v, (B, heads, Lk, C // heads), ctx, "v")
+    status = load_library().sdattn_project_kv(
+        _dev(ctx, "ctx"), _dev(wk, "wk"), _dev(wv, "wv"), _dev(k, "k"), _dev(v, "v"),
+        B, Lk, Cc, C, heads, _dtype_code(ctx), _stream(stream))
+    _check("sdattn_project_kv", status)
+    return k, v
+
+
+def attention_block_kv(x, wq, k, v, wo, bo, out, workspace, scale, stream=None):
+    """The attention block with K and V given in heads layout [B, H, Lk, C/H];
+    workspace of at least attention_block_workspace(B, Lq, 0, C) bytes."""
+    B, Lq, C = x.shape
+    H, Lk = k.shape[1], k.shape[2]
+    _expect(k, (B, H, Lk, C // H), x, "k")
+    _expect(v, k.shape, x, "v")
+    for t, shape, name in ((wq, (C, C), "wq"), (wo, (C, C), "wo"), (out, (B, Lq, C), "out")):
+        _expect(t, shape, x, name)
+    if bo is not None:
+        _expect(bo, (C,), x, "bo")
+    status = load_library().sdattn_attention_block_kv(
+        _dev(x, "x"), _dev(wq, "wq"), _dev(k, "k"), _dev(v, "v"), _dev(wo, "wo"),
+        _dev(bo, "bo") if bo is not None else None, _dev(out, "out"), _dev(workspace, "workspace"),
+        workspace.numel() * workspace.element_size(), B, Lq, Lk, C, H, ctypes.c_float(scale),
+        _dtype_code(x), _stream(stream))
+    _check("sdattn_attention_block_kv", status)
     return out

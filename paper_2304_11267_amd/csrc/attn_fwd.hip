@@ -98,11 +98,11 @@ __device__ __forceinline__ u32x2 lds_read_tr(const char* p) {
     return __builtin_bit_cast(u32x2, v);
 }
 
-template <int ET, int D, bool STATS>
+template <int ET, int D, bool STATS, bool OROWS>
 __global__ __launch_bounds__(Geom<D>::kThreads, Geom<D>::kWavesPerSimd) void attn_fwd_lds_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     uint16_t* __restrict__ O, float* __restrict__ LS, int Lq, int Lk, float scale_abs, float c,
-    int neg, int nqb) {
+    int neg, int nqb, int oh) {
     using G = Geom<D>;
     constexpr int DK = G::DK;
     constexpr int DN = G::DN;
@@ -562,7 +562,8 @@ __global__ __launch_bounds__(Geom<D>::kThreads, Geom<D>::kWavesPerSimd) void att
         const float inv = 1.0f / l;
         const int qrow = q0 + 32 * j + l32;
         if (qrow < Lq) {
-            uint16_t* orow = O + ((size_t)bh * Lq + qrow) * D;
+            uint16_t* orow = OROWS ? out_base(O, bh, Lq, D, oh) + (size_t)qrow * out_stride(D, oh)
+                                   : O + ((size_t)bh * Lq + qrow) * D;
 #pragma unroll
             for (int n = 0; n < DN; ++n)
 #pragma unroll
@@ -596,18 +597,25 @@ hipError_t launch_d(const AttnArgs& a) {
         const float scale_abs = a.scale < 0 ? -a.scale : a.scale;
         const float c = scale_abs * kLog2e;
         static const hipError_t attr0 = hipFuncSetAttribute(
-            reinterpret_cast<const void*>(&attn_fwd_lds_kernel<ET, D, false>),
+            reinterpret_cast<const void*>(&attn_fwd_lds_kernel<ET, D, false, false>),
             hipFuncAttributeMaxDynamicSharedMemorySize, G::kLdsBytes);
         static const hipError_t attr1 = hipFuncSetAttribute(
-            reinterpret_cast<const void*>(&attn_fwd_lds_kernel<ET, D, true>),
+            reinterpret_cast<const void*>(&attn_fwd_lds_kernel<ET, D, true, false>),
+            hipFuncAttributeMaxDynamicSharedMemorySize, G::kLdsBytes);
+        static const hipError_t attr2 = hipFuncSetAttribute(
+            reinterpret_cast<const void*>(&attn_fwd_lds_kernel<ET, D, false, true>),
             hipFuncAttributeMaxDynamicSharedMemorySize, G::kLdsBytes);
         if (attr0 != hipSuccess) return attr0;
         if (attr1 != hipSuccess) return attr1;
-        auto kern = a.ls ? attn_fwd_lds_kernel<ET, D, true> : attn_fwd_lds_kernel<ET, D, false>;
+        if (attr2 != hipSuccess) return attr2;
+        if (a.ls && a.o_rows) return hipErrorInvalidValue;   // no caller asks for both
+        auto kern = a.ls       ? attn_fwd_lds_kernel<ET, D, true, false>
+                    : a.o_rows ? attn_fwd_lds_kernel<ET, D, false, true>
+                               : attn_fwd_lds_kernel<ET, D, false, false>;
         hipLaunchKernelGGL(kern, dim3((unsigned)nblk), dim3(G::kThreads),
                            G::kLdsBytes, (hipStream_t)a.stream, (const uint16_t*)a.q,
                            (const uint16_t*)a.k, (const uint16_t*)a.v, (uint16_t*)a.out, a.ls,
-                           a.Lq, a.Lk, scale_abs, c, a.scale < 0 ? 1 : 0, nqb);
+                           a.Lq, a.Lk, scale_abs, c, a.scale < 0 ? 1 : 0, nqb, a.o_rows ? a.H : 0);
         return hipGetLastError();
     }
 }

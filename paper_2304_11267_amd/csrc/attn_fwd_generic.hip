@@ -59,7 +59,7 @@ template <int ET, int DK>
 __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     uint16_t* __restrict__ O, float* __restrict__ LS, int Lq, int Lk, int D, float scale_abs,
-    float c, int neg, int nqb) {
+    float c, int neg, int nqb, int oh) {
     constexpr int DN = (DK + 1) / 2;       // 32-wide d tiles of O^T
     constexpr int DNP = DN * 32;           // padded d rows of V^T
     constexpr int KCH = (kKB * 2 * DK + kThreads - 1) / kThreads;        // 16-byte K chunks per thread
@@ -306,7 +306,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(
     }
     const float inv = 1.0f / l;
     if (qrow < Lq) {
-        uint16_t* orow = O + ((size_t)bh * Lq + qrow) * D;
+        uint16_t* orow = out_base(O, bh, Lq, D, oh) + (size_t)qrow * out_stride(D, oh);
 #pragma unroll
         for (int n = 0; n < DN; ++n)
 #pragma unroll
@@ -353,7 +353,7 @@ hipError_t launch_dk(const AttnArgs& a) {
     hipLaunchKernelGGL((attn_fwd_kernel<ET, DK>), dim3((unsigned)nblk), dim3(kThreads), lds,
                        (hipStream_t)a.stream, (const uint16_t*)a.q, (const uint16_t*)a.k,
                        (const uint16_t*)a.v, (uint16_t*)a.out, a.ls, a.Lq, a.Lk, a.D, scale_abs, c,
-                       a.scale < 0 ? 1 : 0, nqb);
+                       a.scale < 0 ? 1 : 0, nqb, a.o_rows ? a.H : 0);
     return hipGetLastError();
 }
 

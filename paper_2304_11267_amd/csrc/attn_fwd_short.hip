@@ -74,7 +74,7 @@ template <int ET, int D, int NS, int W>
 __global__ __launch_bounds__(W * 64) void attn_fwd_short_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     uint16_t* __restrict__ O, int Lq, int Lk, float c, int nqb, int nblk, int neg,
-    float* __restrict__ LS, float scale_abs) {
+    float* __restrict__ LS, float scale_abs, int oh) {
     using G = ShortGeom<D, NS, W>;
     constexpr int kThreads = W * 64;
     constexpr int DK = G::DK;
@@ -275,11 +275,24 @@ __global__ __launch_bounds__(W * 64) void attn_fwd_short_kernel(
             }
         }
     {
-        char* os = (char*)(O + ((size_t)bh * Lq + q0) * D);
+        if (oh == 0) {   // the strip's rows are contiguous in O
+            char* os = (char*)(O + ((size_t)bh * Lq + q0) * D);
 #pragma unroll
-        for (int i = 0; i < G::kStripChunks; ++i) {
-            const int byte = i * 1024 + lane * 16;
-            if (byte < strip_bytes) *(u32x4*)(os + byte) = *(const u32x4*)(stage + byte);
+            for (int i = 0; i < G::kStripChunks; ++i) {
+                const int byte = i * 1024 + lane * 16;
+                if (byte < strip_bytes) *(u32x4*)(os + byte) = *(const u32x4*)(stage + byte);
+            }
+        } else {         // row r of the strip is token q0 + r's slice of channels h*D .. h*D + D - 1
+            uint16_t* ob = out_base(O, bh, Lq, D, oh) + (size_t)q0 * out_stride(D, oh);
+#pragma unroll
+            for (int i = 0; i < G::kStripChunks; ++i) {
+                const int byte = i * 1024 + lane * 16;
+                if (byte < strip_bytes) {
+                    const int r = byte / (2 * D), col = byte - r * (2 * D);
+                    *(u32x4*)((char*)(ob + (size_t)r * out_stride(D, oh)) + col) =
+                        *(const u32x4*)(stage + byte);
+                }
+            }
         }
     }
     if (LS && half == 0 && qvalid) {
@@ -304,7 +317,7 @@ hipError_t launch_short_dnw(const AttnArgs& a) {
     hipLaunchKernelGGL((attn_fwd_short_kernel<ET, D, NS, W>), dim3((unsigned)nblk), dim3(W * 64),
                        G::kLdsBytes, (hipStream_t)a.stream, (const uint16_t*)a.q,
                        (const uint16_t*)a.k, (const uint16_t*)a.v, (uint16_t*)a.out, a.Lq, a.Lk, c,
-                       nqb, (int)nblk, a.scale < 0 ? 1 : 0, a.ls, scale_abs);
+                       nqb, (int)nblk, a.scale < 0 ? 1 : 0, a.ls, scale_abs, a.o_rows ? a.H : 0);
     return hipGetLastError();
 }
 

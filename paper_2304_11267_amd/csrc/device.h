@@ -121,4 +121,14 @@ __device__ __forceinline__ float half_partner(float x, int half) {
 
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
 
+// Where query row i of head bh = b*H + h goes in O: out_base(O, ...) + i * out_stride.
+// oh == 0: O is [B, H, Lq, D]; oh == H: O is [B, Lq, H*D] (the heads merged
+// into token rows).
+__device__ __forceinline__ uint16_t* out_base(uint16_t* O, int bh, int Lq, int D, int oh) {
+    if (oh == 0) return O + (size_t)bh * Lq * D;
+    const int b = bh / oh;
+    return O + ((size_t)b * Lq * oh + (bh - b * oh)) * D;
+}
+__device__ __forceinline__ size_t out_stride(int D, int oh) { return oh == 0 ? (size_t)D : (size_t)oh * D; }
+
 }  // namespace sdattn

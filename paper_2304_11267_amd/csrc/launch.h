@@ -15,6 +15,7 @@ struct AttnArgs {
     float scale;
     int dtype;      // ElemType: kF16 or kBF16
     void* stream;
+    int o_rows = 0; // nonzero: out is [B, Lq, H*D] (heads merged) instead of [B, H, Lq, D]
 };
 
 // Number of workgroups the attention kernels launch for these sizes.

@@ -262,19 +262,30 @@ __global__ __launch_bounds__(256) void linear_kernel(const LinGroup grp) {
             }
     }
     lds_barrier();
-    // 16 bytes per lane: chunk q = tid + 256j is tile row q / 8, channels
-    // 8 (q % 8) .. + 7 (inside one head, as head widths are multiples of 8)
-    uint16_t* __restrict__ Y = P.y;
-    const int yhw = P.yhw;
-    const float inv_yhw = 1.0f / (float)yhw;
+    // 16 bytes per lane: chunk q = tid + 256j is tile row q / 8 + 32j, channels
+    // n = n0 + 8 (q % 8) .. + 7 (inside one head, as head widths are multiples
+    // of 8).  The channel offset is the same for all j; the row's batch and
+    // token advance by 32 tokens per j.
+    const int c8 = threadIdx.x & 7;
+    const int n = n0 + 8 * c8;
+    const int r0 = threadIdx.x >> 3;
+    if (n < N) {
+        const int yhw = P.yhw;
+        uint16_t* __restrict__ Yc = P.y + chan_offset<YH>(n, L, yhw, 1.0f / (float)yhw);
+        int b = (m0 + r0) / L, l = (m0 + r0) - b * L;   // token row m = b*L + l
 #pragma unroll
-    for (int j = 0; j < kBM * kBN / 8 / 256; ++j) {
-        const int q = (int)threadIdx.x + 256 * j;
-        const int r = q >> 3, c8 = q & 7;
-        const int m = m0 + r, n = n0 + 8 * c8;
-        if (m < M && n < N) {
-            const u32x4 v = *(const u32x4*)(smem + r * kOutStride + c8 * 16);
-            *(u32x4*)(Y + row_base<YH>(m, L, N, yhw) + chan_offset<YH>(n, L, yhw, inv_yhw)) = v;
+        for (int j = 0; j < kBM * kBN / 8 / 256; ++j) {
+            const int r = r0 + 32 * j;
+            if (m0 + r < M) {
+                const u32x4 v = *(const u32x4*)(smem + r * kOutStride + c8 * 16);
+                const size_t row = YH ? ((size_t)b * (N / yhw) * L + l) * yhw : (size_t)(m0 + r) * N;
+                *(u32x4*)(Yc + row) = v;
+            }
+            l += 32;
+            while (l >= L) {
+                l -= L;
+                ++b;
+            }
         }
     }
 }

@@ -135,7 +135,7 @@ int check_linear(const void* x, const void* w, const void* bias, void* y, int B,
     return SDATTN_OK;
 }
 
-// Q, K, V, O in heads layout, each rounded up to 256 bytes
+// Q, K, V (heads layout) and O (heads merged), each rounded up to 256 bytes
 long long block_part(long long elems) { return (2 * elems + 255) / 256 * 256; }
 
 }  // namespace
@@ -217,7 +217,8 @@ int sdattn_linear(const void* x, const void* w, const void* bias, void* y, int B
 }
 
 long long sdattn_attention_block_workspace(int B, int Lq, int Lk, int C) {
-    const long long nq = checked_mul({B, Lq, C}), nk = checked_mul({B, Lk, C});
+    // Lk == 0: Q and O only (sdattn_attention_block_kv)
+    const long long nq = checked_mul({B, Lq, C}), nk = Lk == 0 ? 0 : checked_mul({B, Lk, C});
     if (nq < 0 || nk < 0) return -1;
     return 2 * block_part(nq) + 2 * block_part(nk);
 }
@@ -259,7 +260,7 @@ int sdattn_attention_block(const void* x, const void* ctx, const void* wq, const
                            (int)dtype, stream, &pk)) != SDATTN_OK ||
         (st = check_linear(ctx, wv, nullptr, v, B, Lk, Cc, C, H, SDATTN_ROWS, SDATTN_HEADS,
                            (int)dtype, stream, &pv)) != SDATTN_OK ||
-        (st = check_linear(o, wo, bo, out, B, Lq, C, C, H, SDATTN_HEADS, SDATTN_ROWS, (int)dtype,
+        (st = check_linear(o, wo, bo, out, B, Lq, C, C, H, SDATTN_ROWS, SDATTN_ROWS, (int)dtype,
                            stream, &po)) != SDATTN_OK)
         return st;
     if ((st = check_attention(q, k, v, o, nullptr, B, H, Lq, Lk, D, scale, (int)dtype)) != SDATTN_OK)
@@ -268,7 +269,69 @@ int sdattn_attention_block(const void* x, const void* ctx, const void* wq, const
     hipError_t e;
     const sdattn::LinearArgs qkv[3] = {pq, pk, pv};
     if ((e = sdattn::launch_linear_group(qkv, 3)) != hipSuccess) return finish(e);
-    sdattn::AttnArgs aa{q, k, v, o, nullptr, B, H, Lq, Lk, D, scale, (int)dtype, stream};
+    // O leaves the attention with the heads merged ([B, Lq, C]), as the output
+    // projection reads it
+    sdattn::AttnArgs aa{q, k, v, o, nullptr, B, H, Lq, Lk, D, scale, (int)dtype, stream, 1};
+    if ((e = sdattn::launch_attn_fwd(aa)) != hipSuccess) return finish(e);
+    return finish(sdattn::launch_linear(po));
+}
+
+int sdattn_project_kv(const void* ctx, const void* wk, const void* wv, void* k, void* v, int B,
+                      int Lk, int Cc, int C, int H, sdattn_dtype dtype, void* stream) {
+    if (!ctx || !wk || !wv || !k || !v) return SDATTN_ERR_INVALID_ARG;
+    if (B < 1 || Lk < 1 || C < 1 || Cc < 1 || H < 1 || C % H != 0) return SDATTN_ERR_INVALID_ARG;
+    sdattn::LinearArgs kv[2];
+    int st;
+    if ((st = check_linear(ctx, wk, nullptr, k, B, Lk, Cc, C, H, SDATTN_ROWS, SDATTN_HEADS,
+                           (int)dtype, stream, &kv[0])) != SDATTN_OK ||
+        (st = check_linear(ctx, wv, nullptr, v, B, Lk, Cc, C, H, SDATTN_ROWS, SDATTN_HEADS,
+                           (int)dtype, stream, &kv[1])) != SDATTN_OK)
+        return st;
+    const unsigned long long kb = 2ULL * B * Lk * C;
+    if (overlap(k, kb, v, kb) || overlap(k, kb, wv, 2ULL * C * Cc) ||
+        overlap(v, kb, wk, 2ULL * C * Cc))
+        return SDATTN_ERR_INVALID_ARG;
+    (void)hipGetLastError();
+    return finish(sdattn::launch_linear_group(kv, 2));
+}
+
+int sdattn_attention_block_kv(const void* x, const void* wq, const void* k, const void* v,
+                              const void* wo, const void* bo, void* out, void* workspace,
+                              long long workspace_bytes, int B, int Lq, int Lk, int C, int H,
+                              float scale, sdattn_dtype dtype, void* stream) {
+    if (!x || !wq || !k || !v || !wo || !out || !workspace) return SDATTN_ERR_INVALID_ARG;
+    if (B < 1 || Lq < 1 || Lk < 1 || C < 1 || H < 1 || C % H != 0) return SDATTN_ERR_INVALID_ARG;
+    const long long need = sdattn_attention_block_workspace(B, Lq, 0, C);
+    if (need < 0) return SDATTN_ERR_UNSUPPORTED;
+    if (workspace_bytes < need) return SDATTN_ERR_INVALID_ARG;
+    if (!aligned(workspace, 16)) return SDATTN_ERR_MISALIGNED;
+    const int D = C / H;
+    void* q = workspace;
+    void* o = (char*)workspace + block_part((long long)B * Lq * C);
+    const unsigned long long ob = 2ULL * B * Lq * C;
+    const void* ins[] = {x, wq, k, v, wo, bo};
+    const unsigned long long insz[] = {2ULL * B * Lq * C, 2ULL * C * C, 2ULL * B * Lk * C,
+                                       2ULL * B * Lk * C, 2ULL * C * C, 2ULL * C};
+    for (int i = 0; i < 6; ++i) {
+        if (!ins[i]) continue;
+        if (overlap(ins[i], insz[i], workspace, (unsigned long long)need) ||
+            overlap(ins[i], insz[i], out, ob))
+            return SDATTN_ERR_INVALID_ARG;
+    }
+    if (overlap(out, ob, workspace, (unsigned long long)need)) return SDATTN_ERR_INVALID_ARG;
+    sdattn::LinearArgs pq, po;
+    int st;
+    if ((st = check_linear(x, wq, nullptr, q, B, Lq, C, C, H, SDATTN_ROWS, SDATTN_HEADS, (int)dtype,
+                           stream, &pq)) != SDATTN_OK ||
+        (st = check_linear(o, wo, bo, out, B, Lq, C, C, H, SDATTN_ROWS, SDATTN_ROWS, (int)dtype,
+                           stream, &po)) != SDATTN_OK)
+        return st;
+    if ((st = check_attention(q, k, v, o, nullptr, B, H, Lq, Lk, D, scale, (int)dtype)) != SDATTN_OK)
+        return st;
+    (void)hipGetLastError();
+    hipError_t e;
+    if ((e = sdattn::launch_linear(pq)) != hipSuccess) return finish(e);
+    sdattn::AttnArgs aa{q, k, v, o, nullptr, B, H, Lq, Lk, D, scale, (int)dtype, stream, 1};
     if ((e = sdattn::launch_attn_fwd(aa)) != hipSuccess) return finish(e);
     return finish(sdattn::launch_linear(po));
 }

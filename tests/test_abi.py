@@ -227,3 +227,39 @@ def test_attention_block_checks(lib):
     assert blk(lib, scale=float("inf")) == INVALID
     assert blk(lib, out=ctypes.c_void_p(0x60000000 + 4096)) == INVALID   # out inside the workspace
     assert blk(lib, x=ctypes.c_void_p(0x60000000 + 1024)) == INVALID     # x inside the workspace
+
+
+def test_project_kv_checks(lib):
+    W1, W2 = ctypes.c_void_p(0x71000000), ctypes.c_void_p(0x72000000)
+
+    def pkv(ctx=KA, wk=W1, wv=W2, k=QA, v=VA, B=2, Lk=77, Cc=768, C=320, H=8, dtype=F16):
+        return lib.sdattn_project_kv(ctx, wk, wv, k, v, B, Lk, Cc, C, H, dtype, None)
+    for field in ("ctx", "wk", "wv", "k", "v"):
+        assert pkv(**{field: None}) == INVALID
+    assert pkv(H=0) == INVALID
+    assert pkv(C=321) == INVALID                        # heads do not divide C
+    assert pkv(C=96) == UNSUPPORTED                     # head width 12
+    assert pkv(Cc=770) == UNSUPPORTED                   # context channels % 8
+    assert pkv(v=ctypes.c_void_p(0x10000000 + 4096)) == INVALID   # v overlaps k
+    assert pkv(k=ctypes.c_void_p(0x10000008)) == MISALIGNED
+
+
+def test_attention_block_kv_checks(lib):
+    def bkv(ws=ctypes.c_void_p(0x60000000), wsb=1 << 26, **kw):
+        a = dict(x=QA, wq=ctypes.c_void_p(0x70000000), k=KA, v=VA, wo=ctypes.c_void_p(0x73000000),
+                 bo=ctypes.c_void_p(0x74000000), out=OA, B=2, Lq=64, Lk=77, C=320, H=8,
+                 scale=0.158, dtype=F16)
+        a.update(kw)
+        return lib.sdattn_attention_block_kv(a["x"], a["wq"], a["k"], a["v"], a["wo"], a["bo"],
+                                             a["out"], ws, wsb, a["B"], a["Lq"], a["Lk"], a["C"],
+                                             a["H"], ctypes.c_float(a["scale"]), a["dtype"], None)
+    need = lib.sdattn_attention_block_workspace(2, 64, 0, 320)
+    assert need == 2 * ((2 * 2 * 64 * 320 + 255) // 256 * 256)
+    assert bkv(wsb=need - 1) == INVALID
+    for field in ("x", "wq", "k", "v", "wo", "out"):
+        assert bkv(**{field: None}) == INVALID
+    assert bkv(ws=None) == INVALID
+    assert bkv(C=321) == INVALID
+    assert bkv(C=96) == UNSUPPORTED
+    assert bkv(scale=float("nan")) == INVALID
+    assert bkv(k=ctypes.c_void_p(0x60000000 + 512)) == INVALID   # k inside the workspace

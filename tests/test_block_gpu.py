@@ -132,8 +132,11 @@ def rounded_chain(inputs, H, scale, rows=None):
     return oracle.linear(o16, wo, bo)
 
 
+# (B, Lq, Lk, C, Cc, H, self): short-key kernel (Lk = 77, 64), tiled kernel (Lk = 200),
+# the general kernel (head width 16 with 150 keys; 256 with 120 keys)
 @pytest.mark.parametrize("shape", [(2, 37, 77, 320, 768, 8, False), (1, 200, 200, 320, 320, 8, True),
-                                   (2, 64, 64, 1280, 1280, 8, True), (1, 130, 77, 640, 768, 8, False)],
+                                   (2, 64, 64, 1280, 1280, 8, True), (1, 130, 77, 640, 768, 8, False),
+                                   (1, 150, 150, 128, 128, 8, True), (1, 100, 120, 2048, 2048, 8, True)],
                          ids=lambda s: "x".join(map(str, s)))
 def test_block_small_full(shape):
     B, Lq, Lk, C, Cc, H, self_attn = shape
@@ -158,3 +161,34 @@ def test_block_unet_sampled_rows(name, per_b):
     rows = np.sort(np.concatenate([b * case.Lq + rng.choice(case.Lq, size=per_b, replace=False)
                                    for b in range(case.B)]))
     assert_close(g[rows], rounded_chain(inputs, case.H, case.scale, rows=rows), what=name)
+
+
+@pytest.mark.parametrize("name", ["blk64_cross", "blk16_cross"])
+def test_cached_context_block(name):
+    """K and V of the text context computed once (project_kv), then the per-step
+    block with them: K and V match the oracle's projections, the output matches
+    the oracle chain, and both equal the one-call block bit for bit."""
+    import torch
+    case = wl.BLOCK_CASES[name]
+    inputs = wl.block_inputs(case)
+    x, ctx, wq, wk, wv, wo, bo = (to_device(t) for t in inputs)
+    D = case.C // case.H
+    k = torch.empty(case.B, case.H, case.Lk, D, dtype=torch.float16, device="cuda")
+    v = torch.empty_like(k)
+    sd.project_kv(ctx, wk, wv, k, v, case.H)
+    ws = torch.empty(sd.attention_block_workspace(case.B, case.Lq, 0, case.C), dtype=torch.uint8,
+                     device="cuda")
+    out = torch.empty(case.B, case.Lq, case.C, dtype=torch.float16, device="cuda")
+    sd.attention_block_kv(x, wq, k, v, wo, bo, out, ws, case.scale)
+    torch.cuda.synchronize()
+    for t, w in ((k, inputs[3]), (v, inputs[4])):
+        r = oracle.linear(inputs[1], w)
+        bound = lin_bound(inputs[1].astype(np.float64), w.astype(np.float64), r)
+        assert np.all(np.abs(rows_of(to_host64(t)) - r) <= bound)
+    g = to_host64(out).reshape(-1, case.C)
+    rng = np.random.default_rng(case.seed + 9)
+    rows = np.sort(np.concatenate([b * case.Lq + rng.choice(case.Lq, size=64, replace=False)
+                                   for b in range(case.B)]))
+    assert_close(g[rows], rounded_chain(inputs, case.H, case.scale, rows=rows), what=name)
+    full = gpu_block(inputs, case.H, case.scale).reshape(-1, case.C)
+    assert np.array_equal(full, g)

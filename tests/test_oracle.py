@@ -494,6 +494,20 @@ def test_linear_matches_numpy_matmul():
     assert np.max(np.abs(oracle.linear(x, w) - (ref - b.astype(np.float64)))) <= 1e-13 * np.abs(ref).max()
 
 
+def test_linear_closed_forms():
+    rng = np.random.default_rng(64)
+    x = _rand16(rng, (2, 3, 16))
+    eye = np.eye(16, dtype=np.float16)
+    assert np.array_equal(oracle.linear(x, eye), x.astype(np.float64))
+    # w picks and scales single input channels: y[..., n] = 2 x[..., 15 - n]
+    sel = np.zeros((16, 16), dtype=np.float16)
+    sel[np.arange(16), 15 - np.arange(16)] = 2.0
+    assert np.array_equal(oracle.linear(x, sel), 2.0 * x.astype(np.float64)[..., ::-1])
+    b = _rand16(rng, (8,))
+    w = _rand16(rng, (8, 16))
+    assert np.array_equal(oracle.linear(np.zeros_like(x), w, b)[1, 2], b.astype(np.float64))
+
+
 def test_attention_block_matches_torch_fp64():
     torch = pytest.importorskip("torch")
     x, ctx, (wq, wk, wv, wo), bo = _blk_inputs(61)

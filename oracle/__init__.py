@@ -16,6 +16,9 @@ passages of the paper each function follows):
   O = exp(A - L) / S times V.
 * :func:`linear` and :func:`attention_block` -- the projections around the
   attention in SD's transformer blocks and the whole multi-head block.
+* :func:`group_norm`, :func:`gelu` and :func:`geglu` -- the specialised
+  kernels of Sec. 3.1: group normalisation (Eq. 1) and GELU (Eq. 2) with its
+  split and multiply.
 
 Inputs are numpy arrays: float16, float32, float64, or bfloat16 passed as a
 uint16 bit-pattern array with ``dtype="bf16"``.
@@ -55,6 +58,14 @@ def _load():
         lib.oracle_attention_block_f64.argtypes = [vp, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32,
                                                    i32, i32, i32, f32, vp, i64, i32, vp]
         lib.oracle_attention_block_f64.restype = i32
+        f64 = ctypes.c_double
+        lib.oracle_group_norm_f64.argtypes = [vp, i32, vp, vp, i32, i32, i64, i32, f64, i32, vp,
+                                              vp, vp]
+        lib.oracle_group_norm_f64.restype = i32
+        lib.oracle_gelu_f64.argtypes = [vp, i32, i64, vp]
+        lib.oracle_gelu_f64.restype = i32
+        lib.oracle_geglu_f64.argtypes = [vp, i32, i64, i32, i32, vp]
+        lib.oracle_geglu_f64.restype = i32
         lib.oracle_widen.argtypes = [vp, i32, i64, vp]
         lib.oracle_widen.restype = i32
         lib.oracle_num_threads.argtypes = [i32]
@@ -250,3 +261,57 @@ def attention_block(x, ctx, wq, wk, wv, wo, bo, heads, scale, rows=None, dtype=N
     if rc != 0:
         raise ValueError("oracle_attention_block_f64 rejected its arguments")
     return out.reshape(B, Lq, C) if rows is None else out
+
+
+def group_norm(x, groups, gamma=None, beta=None, eps=1e-5, dtype=None, nthreads=0):
+    """Group normalisation (Eq. 1 with eps and the per-channel affine terms) in
+    fp64 of x [B, C, ...] (channel-major; the trailing axes are the pixels).
+
+    eps is rounded to fp32 first (the value the GPU receives).
+    Returns (y, mean, rstd): y like x, mean and rstd [B, groups].
+    """
+    x = np.ascontiguousarray(x)
+    B, C = x.shape[:2]
+    HW = int(np.prod(x.shape[2:])) if x.ndim > 2 else 1
+    code = _code(x, dtype)
+    gp = bp = None
+    for t in (gamma, beta):
+        if t is not None and (t.shape != (C,) or t.dtype != x.dtype):
+            raise ValueError("gamma and beta must be [C] of x's type")
+    if gamma is not None:
+        gamma = np.ascontiguousarray(gamma)
+        gp = _ptr(gamma)
+    if beta is not None:
+        beta = np.ascontiguousarray(beta)
+        bp = _ptr(beta)
+    y = np.empty(x.shape, dtype=np.float64)
+    mean = np.empty((B, groups), dtype=np.float64)
+    rstd = np.empty((B, groups), dtype=np.float64)
+    rc = _load().oracle_group_norm_f64(_ptr(x), code, gp, bp, B, C, HW, groups,
+                                       float(np.float32(eps)), int(nthreads), _ptr(y), _ptr(mean),
+                                       _ptr(rstd))
+    if rc != 0:
+        raise ValueError("oracle_group_norm_f64 rejected its arguments")
+    return y, mean, rstd
+
+
+def gelu(x, dtype=None):
+    """GELU of Eq. 2 element-wise in fp64 (erf form)."""
+    x = np.ascontiguousarray(x)
+    out = np.empty(x.shape, dtype=np.float64)
+    if _load().oracle_gelu_f64(_ptr(x), _code(x, dtype), x.size, _ptr(out)) != 0:
+        raise ValueError("oracle_gelu_f64 rejected its arguments")
+    return out
+
+
+def geglu(h, dtype=None, nthreads=0):
+    """h [..., 2F] -> h[..., :F] * GELU(h[..., F:]) in fp64."""
+    h = np.ascontiguousarray(h)
+    if h.shape[-1] % 2:
+        raise ValueError("the last axis must have an even length")
+    F = h.shape[-1] // 2
+    M = h.size // (2 * F)
+    out = np.empty(h.shape[:-1] + (F,), dtype=np.float64)
+    if _load().oracle_geglu_f64(_ptr(h), _code(h, dtype), M, F, int(nthreads), _ptr(out)) != 0:
+        raise ValueError("oracle_geglu_f64 rejected its arguments")
+    return out

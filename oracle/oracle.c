@@ -25,6 +25,11 @@
  * definition.  Rows are independent, so OpenMP splits the work by row; the
  * result does not depend on the thread count.
  *
+ * Also the steps around the attention (the projections and the multi-head
+ * block) and the specialised kernels of Sec. 3.1 (group normalisation, Eq. 1;
+ * GELU, Eq. 2, with its split and multiply), each written out from its
+ * definition below.
+ *
  * Build: gcc -O2 -fopenmp -fPIC -shared (no -ffast-math).
  */
 #include <math.h>
@@ -437,4 +442,88 @@ int oracle_attention_block_f64(const void *x, const void *ctx, const void *wq, c
     free(Kf);
     free(Vf);
     return bad;
+}
+
+/*
+ * Group normalisation (Sec. 3.1, Eq. 1) of feature maps x [B][C][HW] (the
+ * channel-major layout of the UNet's convolution outputs) of type `dtype`.
+ * The C channels form G groups of C/G consecutive channels; group (b, g)
+ * holds the (C/G)*HW values of channels g*C/G .. (g+1)*C/G - 1 of batch b.
+ *   mu  = the group's mean,  var = the mean of (x - mu)^2  (a second pass),
+ *   y_i = (x_i - mu) / sqrt(var + eps) * gamma_c + beta_c   (c: x_i's channel).
+ * Eq. 1 is the case eps = 0 without the per-channel affine terms; gamma and
+ * beta (type `dtype`, [C]) may be NULL for 1 and 0.  mean and rstd, when not
+ * NULL, receive mu and 1/sqrt(var + eps) per group, [B][G].
+ */
+int oracle_group_norm_f64(const void *x, int dtype, const void *gamma, const void *beta, int B,
+                          int C, int64_t HW, int G, double eps, int nthreads, double *y,
+                          double *mean, double *rstd)
+{
+    if (!x || !y || B < 1 || C < 1 || HW < 1 || G < 1 || C % G != 0 || eps < 0.0 ||
+        dtype < OR_F16 || dtype > OR_F64)
+        return 1;
+    const int cpg = C / G;
+    const int64_t n = (int64_t)cpg * HW;
+
+#pragma omp parallel for schedule(static) num_threads(oracle_num_threads(nthreads))
+    for (int64_t bg = 0; bg < (int64_t)B * G; ++bg) {
+        const int64_t base = bg * n;   /* the group's values are contiguous */
+        double s = 0.0;
+        for (int64_t i = 0; i < n; ++i)
+            s += or_elem(x, dtype, base + i);
+        const double mu = s / (double)n;
+        double s2 = 0.0;
+        for (int64_t i = 0; i < n; ++i) {
+            const double d = or_elem(x, dtype, base + i) - mu;
+            s2 += d * d;
+        }
+        const double var = s2 / (double)n;
+        const double inv = 1.0 / sqrt(var + eps);
+        const int g = (int)(bg % G);
+        for (int64_t i = 0; i < n; ++i) {
+            const int c = g * cpg + (int)(i / HW);
+            const double ga = gamma ? or_elem(gamma, dtype, c) : 1.0;
+            const double be = beta ? or_elem(beta, dtype, c) : 0.0;
+            y[base + i] = (or_elem(x, dtype, base + i) - mu) * inv * ga + be;
+        }
+        if (mean)
+            mean[bg] = mu;
+        if (rstd)
+            rstd[bg] = inv;
+    }
+    return 0;
+}
+
+/* GELU of Eq. 2, element-wise: out_i = x_i / 2 * (1 + erf(x_i / sqrt(2))). */
+int oracle_gelu_f64(const void *x, int dtype, int64_t n, double *out)
+{
+    if (!x || !out || n < 0 || dtype < OR_F16 || dtype > OR_F64)
+        return 1;
+    for (int64_t i = 0; i < n; ++i) {
+        const double v = or_elem(x, dtype, i);
+        out[i] = 0.5 * v * (1.0 + erf(v / sqrt(2.0)));
+    }
+    return 0;
+}
+
+/*
+ * The GELU of Eq. 2 with the split and multiply around it (the gated
+ * feed-forward of the transformer block): h [M][2F] of type `dtype` is split
+ * along its last axis into a value half and a gate half,
+ *   out[m][f] = h[m][f] * GELU(h[m][F + f]),   out [M][F] doubles.
+ */
+int oracle_geglu_f64(const void *h, int dtype, int64_t M, int F, int nthreads, double *out)
+{
+    if (!h || !out || M < 1 || F < 1 || dtype < OR_F16 || dtype > OR_F64)
+        return 1;
+
+#pragma omp parallel for schedule(static) num_threads(oracle_num_threads(nthreads))
+    for (int64_t m = 0; m < M; ++m) {
+        for (int f = 0; f < F; ++f) {
+            const double a = or_elem(h, dtype, m * 2 * F + f);
+            const double g = or_elem(h, dtype, m * 2 * F + F + f);
+            out[m * F + f] = a * (0.5 * g * (1.0 + erf(g / sqrt(2.0))));
+        }
+    }
+    return 0;
 }

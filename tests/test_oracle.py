@@ -545,3 +545,109 @@ def test_attention_block_rows_subset():
     rows = np.array([0, 3, 8, 9, 17])
     sub = oracle.attention_block(x, ctx, wq, wk, wv, wo, bo, 2, 0.25, rows=rows)
     assert np.array_equal(sub, full.reshape(-1, full.shape[-1])[rows])
+
+
+# ---- the specialised kernels of Sec. 3.1: group normalisation (Eq. 1) and GELU
+# (Eq. 2) with its split and multiply.  Pinned against torch's fp64 group_norm
+# and exact gelu (independent implementations), closed forms and invariants.
+
+def test_group_norm_matches_torch_fp64():
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(70)
+    for (B, C, H, W, G, eps) in ((2, 32, 5, 7, 8, 1e-5), (1, 12, 4, 4, 3, 1e-6), (3, 6, 1, 1, 6, 1e-5),
+                                 (2, 10, 9, 2, 1, 0.0), (1, 64, 3, 3, 32, 1e-5)):
+        x = (rng.standard_normal((B, C, H, W)) * 2 + 0.5).astype(np.float16)
+        gamma = (1 + 0.3 * rng.standard_normal(C)).astype(np.float16)
+        beta = (0.2 * rng.standard_normal(C)).astype(np.float16)
+        y, mean, rstd = oracle.group_norm(x, G, gamma, beta, eps)
+        e32 = float(np.float32(eps))
+        ref = torch.nn.functional.group_norm(torch.from_numpy(x.astype(np.float64)), G,
+                                             torch.from_numpy(gamma.astype(np.float64)),
+                                             torch.from_numpy(beta.astype(np.float64)), e32).numpy()
+        assert np.max(np.abs(y - ref)) <= 1e-12 * max(1.0, np.abs(ref).max()), (B, C, G)
+        xg = x.astype(np.float64).reshape(B, G, -1)
+        assert np.allclose(mean, xg.mean(axis=2), rtol=0, atol=1e-13)
+        assert np.allclose(rstd, 1 / np.sqrt(xg.var(axis=2) + e32), rtol=1e-12, atol=0)
+
+
+def test_group_norm_closed_forms():
+    B, C, HW, G = 2, 8, 6, 4
+    # a constant group normalises to zero: the output is beta
+    x = np.full((B, C, HW), 3.5, dtype=np.float16)
+    beta = np.arange(C, dtype=np.float16) / 4
+    y, _, _ = oracle.group_norm(x, G, None, beta, 1e-5)
+    assert np.array_equal(y, np.broadcast_to(beta.astype(np.float64)[None, :, None], y.shape))
+    # a group of +a and -a in equal numbers: mean 0, variance a^2, so the output
+    # is +-a / sqrt(a^2 + eps) (+-1 for eps = 0); a small a makes eps visible
+    s = np.where(np.arange(2 * HW) % 2 == 0, 1.0, -1.0).reshape(2, HW)
+    for a, eps in ((0.5, 0.0), (2.0 ** -10, 1e-6), (2.0 ** -8, 1e-5)):
+        x = np.tile((a * s)[None], (B, G, 1)).astype(np.float16)   # [B, C, HW], 2 channels per group
+        y, mean, _ = oracle.group_norm(x, G, None, None, eps)
+        e32 = float(np.float32(eps))
+        want = a * s / np.sqrt(a * a + e32)
+        assert np.allclose(y, np.tile(want[None], (B, G, 1)), rtol=1e-14, atol=0)
+        assert np.array_equal(mean, np.zeros((B, G)))
+
+
+def test_group_norm_invariants():
+    rng = np.random.default_rng(71)
+    B, C, HW, G = 2, 12, 50, 4
+    x = rng.standard_normal((B, C, HW)).astype(np.float16)
+    y, _, rstd = oracle.group_norm(x, G, None, None, 1e-5)
+    yg = y.reshape(B, G, -1)
+    # zero mean and variance var / (var + eps) per group
+    var = 1 / rstd ** 2 - float(np.float32(1e-5))
+    assert np.max(np.abs(yg.mean(axis=2))) <= 1e-14
+    assert np.allclose(yg.var(axis=2), var / (var + float(np.float32(1e-5))), rtol=1e-12)
+    # the affine terms act per channel after the normalisation
+    gamma = (1 + rng.standard_normal(C)).astype(np.float16)
+    beta = rng.standard_normal(C).astype(np.float16)
+    ya, _, _ = oracle.group_norm(x, G, gamma, beta, 1e-5)
+    want = y * gamma.astype(np.float64)[None, :, None] + beta.astype(np.float64)[None, :, None]
+    assert np.max(np.abs(ya - want)) <= 1e-14
+    # the groups are consecutive channel blocks: moving one value inside a group
+    # changes only that group's outputs
+    x2 = x.copy()
+    x2[1, 5, 7] += np.float16(3)
+    y2, _, _ = oracle.group_norm(x2, G, None, None, 1e-5)
+    changed = np.any(y2 != y, axis=2)
+    assert changed[1, 3:6].all() and changed.sum() == 3
+
+
+def test_gelu_known_values_and_identities():
+    torch = pytest.importorskip("torch")
+    # the standard normal CDF at 1 is 0.841344746068542948... (tables)
+    assert abs(oracle.gelu(np.array([1.0]))[0] - 0.8413447460685429) <= 1e-15
+    x = np.linspace(-12, 12, 2001)
+    g = oracle.gelu(x)
+    assert g[1000] == 0.0
+    # GELU(x) - GELU(-x) = x
+    assert np.max(np.abs(g - g[::-1] - x)) <= 1e-14
+    # tails: x for large x, 0 for large -x
+    assert abs(g[-1] - 12.0) <= 1e-30 and abs(g[0]) <= 1e-30
+    # slope 1/2 at 0
+    h = 1e-6
+    d = (oracle.gelu(np.array([h]))[0] - oracle.gelu(np.array([-h]))[0]) / (2 * h)
+    assert abs(d - 0.5) <= 1e-9
+    ref = torch.nn.functional.gelu(torch.from_numpy(x), approximate="none").numpy()
+    assert np.max(np.abs(g - ref)) <= 1e-15
+    # fp16 and bf16 inputs are widened exactly
+    x16 = np.array([-3.5, -0.25, 0.0, 1.0, 6.0], dtype=np.float16)
+    assert np.array_equal(oracle.gelu(x16), oracle.gelu(x16.astype(np.float64)))
+
+
+def test_geglu_split_and_product():
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(72)
+    h = (rng.standard_normal((3, 5, 2 * 24)) * 2).astype(np.float16)
+    out = oracle.geglu(h)
+    ht = torch.from_numpy(h.astype(np.float64))
+    a, gate = ht.chunk(2, dim=-1)
+    ref = (a * torch.nn.functional.gelu(gate, approximate="none")).numpy()
+    assert out.shape == (3, 5, 24)
+    assert np.max(np.abs(out - ref)) <= 1e-14 * max(1.0, np.abs(ref).max())
+    # the first half is the value, the second the gate
+    v = np.concatenate([np.ones((4, 6)), rng.standard_normal((4, 6))], axis=1)
+    assert np.array_equal(oracle.geglu(v), oracle.gelu(v[:, 6:]))
+    big = np.concatenate([rng.standard_normal((4, 6)), np.full((4, 6), 40.0)], axis=1)
+    assert np.array_equal(oracle.geglu(big), big[:, :6] * 40.0)   # GELU(40) = 40 in fp64

@@ -223,6 +223,35 @@ int sdattn_attention_block_kv(const void *x, const void *wq, const void *k, cons
                               long long workspace_bytes, int B, int Lq, int Lk, int C, int H,
                               float scale, sdattn_dtype dtype, void *stream);
 
+/*
+ * Group normalisation, Sec. 3.1 Eq. 1, in one launch with no intermediate
+ * tensor, with the epsilon and per-channel affine terms of the networks that
+ * use it (Eq. 1 itself is eps = 0, gamma = NULL, beta = NULL):
+ *   y = (x - mu_g) / sqrt(var_g + eps) * gamma_c + beta_c
+ * over feature maps x [B, C, HW] (channel-major: the C channels of batch b,
+ * each a contiguous run of HW pixels); group g is channels g*C/G ..
+ * (g+1)*C/G - 1, mu_g and var_g its mean and mean square deviation
+ * (population variance).  fp32 arithmetic, output rounded to nearest even.
+ *
+ *   x, y [B, C, HW] of `dtype` (fp16 or bf16), 16-byte aligned; y may be x
+ *   (in place) but must not overlap it otherwise; gamma, beta [C] of `dtype`
+ *   or NULL (for 1 and 0).  Requirements: C % G == 0; eps finite and >= 0.
+ */
+int sdattn_group_norm(const void *x, const void *gamma, const void *beta, void *y, int B, int C,
+                      long long HW, int G, float eps, sdattn_dtype dtype, void *stream);
+
+/*
+ * GELU, Sec. 3.1 Eq. 2, fused with the split and multiply around it (the gated
+ * feed-forward of the transformer block):
+ *   out[m, f] = h[m, f] * GELU(h[m, F + f]),  GELU(x) = x/2 (1 + erf(x / sqrt 2))
+ * for h [M, 2F] (value half, then gate half) -> out [M, F]; fp32 arithmetic
+ * (erf to within 3e-7), output rounded to nearest even.
+ *
+ *   h, out of `dtype` (fp16 or bf16), 16-byte aligned, not overlapping;
+ *   F % 8 == 0.
+ */
+int sdattn_geglu(const void *h, void *out, long long M, int F, sdattn_dtype dtype, void *stream);
+
 /* Static English text for a status code (never NULL). */
 const char *sdattn_status_str(int status);
 

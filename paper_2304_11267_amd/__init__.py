@@ -8,7 +8,8 @@ falling back to anything else.
 """
 from .binding import (  # noqa: F401
     SdattnError, forward, forward_ex, softmax_rows, logits, softmax_pv, linear,
-    attention_block_workspace, attention_block, project_kv, attention_block_kv, library_path,
+    attention_block_workspace, attention_block, project_kv, attention_block_kv, group_norm, geglu,
+    library_path,
     load_library,
     LAYOUT_ROWS, LAYOUT_HEADS,
     STATUS_OK, STATUS_INVALID_ARG, STATUS_UNSUPPORTED, STATUS_MISALIGNED, STATUS_HIP,

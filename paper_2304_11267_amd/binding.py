@@ -29,6 +29,7 @@ DTYPE_F32 = 2
 EXPORTS = ("sdattn_forward", "sdattn_forward_ex", "sdattn_softmax_rows", "sdattn_logits",
            "sdattn_softmax_pv", "sdattn_linear", "sdattn_attention_block_workspace",
            "sdattn_attention_block", "sdattn_project_kv", "sdattn_attention_block_kv",
+           "sdattn_group_norm", "sdattn_geglu",
            "sdattn_status_str", "sdattn_last_hip_error", "sdattn_version")
 
 LAYOUT_ROWS = 0
@@ -81,6 +82,10 @@ def load_library():
     lib.sdattn_attention_block_kv.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i64, i32, i32, i32,
                                               i32, i32, f32, i32, vp]
     lib.sdattn_attention_block_kv.restype = i32
+    lib.sdattn_group_norm.argtypes = [vp, vp, vp, vp, i32, i32, i64, i32, f32, i32, vp]
+    lib.sdattn_group_norm.restype = i32
+    lib.sdattn_geglu.argtypes = [vp, vp, i64, i32, i32, vp]
+    lib.sdattn_geglu.restype = i32
     lib.sdattn_status_str.argtypes = [i32]
     lib.sdattn_status_str.restype = ctypes.c_char_p
     lib.sdattn_last_hip_error.argtypes = []
@@ -296,4 +301,37 @@ def attention_block_kv(x, wq, k, v, wo, bo, out, workspace, scale, stream=None):
         workspace.numel() * workspace.element_size(), B, Lq, Lk, C, H, ctypes.c_float(scale),
         _dtype_code(x), _stream(stream))
     _check("sdattn_attention_block_kv", status)
+    return out
+
+
+def group_norm(x, groups, y, gamma=None, beta=None, eps=1e-5, stream=None):
+    """Group normalisation of channel-major feature maps x [B, C, ...] into y
+    (same shape; y may be x); gamma, beta [C] or None."""
+    B, C = x.shape[:2]
+    HW = 1
+    for d in x.shape[2:]:
+        HW *= d
+    _expect(y, x.shape, x, "y")
+    for t, name in ((gamma, "gamma"), (beta, "beta")):
+        if t is not None:
+            _expect(t, (C,), x, name)
+    status = load_library().sdattn_group_norm(
+        _dev(x, "x"), _dev(gamma, "gamma") if gamma is not None else None,
+        _dev(beta, "beta") if beta is not None else None, _dev(y, "y"), B, C, HW, groups,
+        ctypes.c_float(eps), _dtype_code(x), _stream(stream))
+    _check("sdattn_group_norm", status)
+    return y
+
+
+def geglu(h, out, stream=None):
+    """out[..., f] = h[..., f] * GELU(h[..., F + f]) for h [..., 2F], out [..., F]."""
+    F2 = h.shape[-1]
+    if F2 % 2:
+        raise ValueError("h's last axis must have an even length")
+    F = F2 // 2
+    _expect(out, tuple(h.shape[:-1]) + (F,), h, "out")
+    M = h.numel() // F2
+    status = load_library().sdattn_geglu(_dev(h, "h"), _dev(out, "out"), M, F, _dtype_code(h),
+                                         _stream(stream))
+    _check("sdattn_geglu", status)
     return out

@@ -84,4 +84,29 @@ hipError_t launch_linear(const LinearArgs& a);
 constexpr int kMaxLinearProblems = 3;
 hipError_t launch_linear_group(const LinearArgs* a, int n);
 
+// Group normalisation and GEGLU (norm_act.hip).
+struct GroupNormArgs {
+    const void* x;        // [B, C, HW]
+    const void* gamma;    // [C] or null
+    const void* beta;     // [C] or null
+    void* y;              // like x (may be x)
+    int B, C;
+    long long HW;
+    int G;
+    float eps;
+    int dtype;
+    void* stream;
+};
+hipError_t launch_group_norm(const GroupNormArgs& a);
+
+struct GegluArgs {
+    const void* h;        // [M, 2F]
+    void* out;            // [M, F]
+    long long M;
+    int F;                // multiple of 8
+    int dtype;
+    void* stream;
+};
+hipError_t launch_geglu(const GegluArgs& a);
+
 }  // namespace sdattn

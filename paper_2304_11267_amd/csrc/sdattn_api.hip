@@ -336,6 +336,43 @@ int sdattn_attention_block_kv(const void* x, const void* wq, const void* k, cons
     return finish(sdattn::launch_linear(po));
 }
 
+int sdattn_group_norm(const void* x, const void* gamma, const void* beta, void* y, int B, int C,
+                      long long HW, int G, float eps, sdattn_dtype dtype, void* stream) {
+    if (!x || !y) return SDATTN_ERR_INVALID_ARG;
+    if (B < 1 || C < 1 || HW < 1 || G < 1 || C % G != 0) return SDATTN_ERR_INVALID_ARG;
+    if (!isfinite(eps) || eps < 0.0f) return SDATTN_ERR_INVALID_ARG;
+    if (dtype != SDATTN_F16 && dtype != SDATTN_BF16)
+        return dtype == SDATTN_F32 ? SDATTN_ERR_UNSUPPORTED : SDATTN_ERR_INVALID_ARG;
+    const long long n = checked_mul({B, C, HW});
+    if (n < 0 || (long long)B * G > INT_MAX) return SDATTN_ERR_UNSUPPORTED;
+    if (!aligned(x, 16) || !aligned(y, 16) || (gamma && !aligned(gamma, 2)) ||
+        (beta && !aligned(beta, 2)))
+        return SDATTN_ERR_MISALIGNED;
+    const unsigned long long nb = 2ULL * n;
+    // y is x itself (in place) or disjoint from it; gamma and beta stay clear of y
+    if (y != x && overlap(y, nb, x, nb)) return SDATTN_ERR_INVALID_ARG;
+    if ((gamma && overlap(y, nb, gamma, 2ULL * C)) || (beta && overlap(y, nb, beta, 2ULL * C)))
+        return SDATTN_ERR_INVALID_ARG;
+    (void)hipGetLastError();
+    sdattn::GroupNormArgs a{x, gamma, beta, y, B, C, HW, G, eps, (int)dtype, stream};
+    return finish(sdattn::launch_group_norm(a));
+}
+
+int sdattn_geglu(const void* h, void* out, long long M, int F, sdattn_dtype dtype, void* stream) {
+    if (!h || !out) return SDATTN_ERR_INVALID_ARG;
+    if (M < 1 || F < 1) return SDATTN_ERR_INVALID_ARG;
+    if (dtype != SDATTN_F16 && dtype != SDATTN_BF16)
+        return dtype == SDATTN_F32 ? SDATTN_ERR_UNSUPPORTED : SDATTN_ERR_INVALID_ARG;
+    if (F % 8 != 0) return SDATTN_ERR_UNSUPPORTED;
+    const long long nh = checked_mul({M, 2LL * F});
+    if (nh < 0) return SDATTN_ERR_UNSUPPORTED;
+    if (!aligned(h, 16) || !aligned(out, 16)) return SDATTN_ERR_MISALIGNED;
+    if (overlap(out, (unsigned long long)nh, h, 2ULL * nh)) return SDATTN_ERR_INVALID_ARG;
+    (void)hipGetLastError();
+    sdattn::GegluArgs a{h, out, M, F, (int)dtype, stream};
+    return finish(sdattn::launch_geglu(a));
+}
+
 const char* sdattn_status_str(int status) {
     switch (status) {
         case SDATTN_OK: return "ok";

@@ -216,3 +216,87 @@ def make_block(B, Lq, Lk, C, Cc, seed, self_attn=False, dtype="f16"):
 
 def block_inputs(case: BlockCase, dtype="f16"):
     return make_block(case.B, case.Lq, case.Lk, case.C, case.Cc, case.seed, case.self_attn, dtype)
+
+
+# Group normalisation and the gated feed-forward around the transformer
+# blocks (Sec. 3.1): SD1.4's feature maps per level (channels x pixels), 32
+# groups; the feed-forward's inner width is 4C, so GEGLU's input has 8C columns.
+GN_GROUPS = 32
+GN_EPS = 1e-5
+
+
+@dataclass(frozen=True)
+class NormCase:
+    name: str
+    B: int
+    C: int
+    HW: int
+    seed: int
+
+    @property
+    def bytes(self) -> int:
+        """Algorithmic HBM bytes: x read once, y written once (2-byte elements)."""
+        return 2 * 2 * self.B * self.C * self.HW
+
+
+@dataclass(frozen=True)
+class GegluCase:
+    name: str
+    M: int          # token rows (B * L)
+    F: int          # output width (4C)
+    seed: int
+
+    @property
+    def bytes(self) -> int:
+        """h read once (2F per row), out written once (F per row), 2-byte elements."""
+        return 2 * 3 * self.M * self.F
+
+
+NORM_CASES = {
+    "gn64": NormCase("gn64", BATCH, 320, 4096, SEED0 + 31),
+    "gn32": NormCase("gn32", BATCH, 640, 1024, SEED0 + 32),
+    "gn16": NormCase("gn16", BATCH, 1280, 256, SEED0 + 33),
+    "gn8": NormCase("gn8", BATCH, 1280, 64, SEED0 + 34),
+    "gn32_cat": NormCase("gn32_cat", BATCH, 960, 1024, SEED0 + 35),   # decoder concat width
+}
+
+GEGLU_CASES = {
+    "geglu64": GegluCase("geglu64", BATCH * 4096, 1280, SEED0 + 41),
+    "geglu32": GegluCase("geglu32", BATCH * 1024, 2560, SEED0 + 42),
+    "geglu16": GegluCase("geglu16", BATCH * 256, 5120, SEED0 + 43),
+}
+
+
+def _cast(a, dtype):
+    if dtype == "f16":
+        return a.astype(np.float16)
+    if dtype == "bf16":
+        return to_bf16_bits(a)
+    raise ValueError(f"unknown dtype {dtype!r}")
+
+
+def make_norm(B, C, HW, seed, dtype="f16"):
+    """x [B, C, HW] with per-channel offsets and scales (x = m_c + s_c z, z ~ N(0,1),
+    m_c ~ N(0, 1), s_c ~ U(0.2, 2)), then gamma ~ 1 + 0.2 N(0,1), beta ~ 0.2 N(0,1),
+    drawn in that order from default_rng(seed) in float32."""
+    rng = np.random.default_rng(seed)
+    m = rng.standard_normal((1, C, 1), dtype=np.float32)
+    s = rng.uniform(0.2, 2.0, size=(1, C, 1)).astype(np.float32)
+    x = m + s * rng.standard_normal((B, C, HW), dtype=np.float32)
+    gamma = 1 + 0.2 * rng.standard_normal(C, dtype=np.float32)
+    beta = 0.2 * rng.standard_normal(C, dtype=np.float32)
+    return tuple(_cast(t, dtype) for t in (x, gamma, beta))
+
+
+def norm_inputs(case: NormCase, dtype="f16"):
+    return make_norm(case.B, case.C, case.HW, case.seed, dtype)
+
+
+def make_geglu(M, F, seed, dtype="f16", sigma=1.5):
+    """h [M, 2F] ~ N(0, sigma^2) from default_rng(seed) in float32."""
+    rng = np.random.default_rng(seed)
+    return _cast(rng.standard_normal((M, 2 * F), dtype=np.float32) * np.float32(sigma), dtype)
+
+
+def geglu_inputs(case: GegluCase, dtype="f16"):
+    return make_geglu(case.M, case.F, case.seed, dtype)

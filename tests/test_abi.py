@@ -263,3 +263,34 @@ def test_attention_block_kv_checks(lib):
     assert bkv(C=96) == UNSUPPORTED
     assert bkv(scale=float("nan")) == INVALID
     assert bkv(k=ctypes.c_void_p(0x60000000 + 512)) == INVALID   # k inside the workspace
+
+
+def test_group_norm_checks(lib):
+    def gn(x=QA, gamma=KA, beta=VA, y=OA, B=2, C=320, HW=4096, G=32, eps=1e-5, dtype=F16):
+        return lib.sdattn_group_norm(x, gamma, beta, y, B, C, HW, G, ctypes.c_float(eps), dtype, None)
+    for field in ("x", "y"):
+        assert gn(**{field: None}) == INVALID
+    for field in ("B", "C", "HW", "G"):
+        assert gn(**{field: 0}) == INVALID
+    assert gn(G=33) == INVALID                          # groups do not divide C
+    assert gn(eps=-1e-5) == INVALID
+    assert gn(eps=float("inf")) == INVALID
+    assert gn(dtype=F32) == UNSUPPORTED
+    assert gn(dtype=7) == INVALID
+    assert gn(x=ctypes.c_void_p(0x10000008)) == MISALIGNED
+    assert gn(gamma=ctypes.c_void_p(0x20000001)) == MISALIGNED
+    assert gn(y=ctypes.c_void_p(0x10000000 + 4096)) == INVALID     # partial overlap with x
+    assert gn(gamma=ctypes.c_void_p(0x40000000 + 64)) == INVALID   # gamma inside y
+
+
+def test_geglu_checks(lib):
+    def ge(h=QA, out=OA, M=8192, F=1280, dtype=F16):
+        return lib.sdattn_geglu(h, out, M, F, dtype, None)
+    for field in ("h", "out"):
+        assert ge(**{field: None}) == INVALID
+    assert ge(M=0) == INVALID
+    assert ge(F=0) == INVALID
+    assert ge(F=1284) == UNSUPPORTED                    # F % 8
+    assert ge(dtype=F32) == UNSUPPORTED
+    assert ge(out=ctypes.c_void_p(0x40000004)) == MISALIGNED
+    assert ge(out=ctypes.c_void_p(0x10000000 + 2 * 1280 * 2)) == INVALID   # out inside h

@@ -4,14 +4,17 @@
 //
 // Group normalisation.  Feature maps are channel-major, [B, C, HW], so group
 // (b, g) -- channels g*C/G .. (g+1)*C/G - 1 of batch b -- is one contiguous
-// run of n = (C/G)*HW values.  One workgroup of 512 threads owns a group.
-// When the run fits in the workgroup's registers (n <= 49152 values, every
-// UNet level: 40960 at 64x64 with 320 channels) it is read once, 16 bytes per
-// lane, and kept: the mean, then the mean square deviation from it (the two
-// passes of the definition, over registers), then y = x*a_c + b_c with
-// a_c = gamma_c / sqrt(var + eps) and b_c = beta_c - mean*a_c, written once.
-// Larger groups (or pixel counts that are not a multiple of 8) take the same
-// three steps reading the run from memory each time.
+// run of n = (C/G)*HW values.  A workgroup of 512 threads reads a group's
+// run once into registers, 16 bytes per lane (n <= 49152 values: every UNet
+// level, 40960 at 64x64 with 320 channels), and keeps it: the mean, then the
+// mean square deviation from it (the two passes of the definition, over
+// registers), then y = x*a_c + b_c with a_c = gamma_c / sqrt(var + eps) and
+// b_c = beta_c - mean*a_c (gamma, beta staged in LDS).  With fewer than 256
+// groups, S = 2 or 4 workgroups share a group, all on one XCD: each computes
+// the statistics from the whole run (the later reads hit that XCD's L2) and
+// writes 1/S of the output, so the launch covers the chip.  Larger groups
+// (or pixel counts that are not a multiple of 8) take the same three steps
+// in one workgroup, reading the run from memory each time.
 //
 // GEGLU.  h [M, 2F] -> out[m, f] = h[m, f] * GELU(h[m, F + f]); 16 bytes of
 // each half per lane, one 16-byte store.  erf comes from the rational
@@ -28,6 +31,7 @@ namespace {
 constexpr int kGnThreads = 512;
 constexpr int kGnChunks = 12;                                 // 16-byte chunks per thread
 constexpr long long kGnResident = (long long)kGnThreads * kGnChunks * 8;   // values
+constexpr int kGnMaxCpg = 1024;   // channels per group the resident kernel stages
 
 template <int ET>
 __device__ __forceinline__ void unpack8(u32x4 v, float* f) {
@@ -60,17 +64,30 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
     return s;
 }
 
-template <int ET>
+template <int ET, int S>
 __global__ __launch_bounds__(kGnThreads) void gn_resident_kernel(
     const uint16_t* X, const uint16_t* __restrict__ Gamma,
-    const uint16_t* __restrict__ Beta, uint16_t* Y, int C, int HW, int G, int n, float eps) {
+    const uint16_t* __restrict__ Beta, uint16_t* Y, int C, int HW, int G, int n, float eps,
+    int ngroups) {
     __shared__ float red[kGnThreads / 64];
-    const int bg = blockIdx.x;
+    __shared__ float gsh[kGnMaxCpg], bsh[kGnMaxCpg];   // the group's gamma and beta
+    // S workgroups per group, all on one XCD (dispatch is round-robin over the
+    // eight XCDs): each reads the whole group (the other S - 1 reads hit that
+    // XCD's L2) and writes the s-th part of the output
+    const int xcd = blockIdx.x % 8, slot = blockIdx.x / 8;
+    const int bg = (slot / S) * 8 + xcd;
+    const int sp = slot % S;
+    if (bg >= ngroups) return;
     const int g = bg % G;
     const int cpg = C / G;
     const size_t base = (size_t)bg * n;
     const int nch = n / 8;
     const int tid = threadIdx.x;
+    const int lo = (int)((long long)nch * sp / S), hi = (int)((long long)nch * (sp + 1) / S);
+    for (int i = tid; i < cpg; i += kGnThreads) {   // read beside x; used after the statistics
+        gsh[i] = Gamma ? to_float<ET>(Gamma[g * cpg + i]) : 1.0f;
+        bsh[i] = Beta ? to_float<ET>(Beta[g * cpg + i]) : 0.0f;
+    }
 
     u32x4 xr[kGnChunks];
 #pragma unroll
@@ -105,12 +122,10 @@ __global__ __launch_bounds__(kGnThreads) void gn_resident_kernel(
 #pragma unroll
     for (int j = 0; j < kGnChunks; ++j) {
         const int q = tid + kGnThreads * j;
-        if (q < nch) {
-            const int c = g * cpg + (8 * q) / HW;   // HW % 8 == 0: one channel per chunk
-            const float ga = Gamma ? to_float<ET>(Gamma[c]) : 1.0f;
-            const float be = Beta ? to_float<ET>(Beta[c]) : 0.0f;
-            const float a = rstd * ga;
-            const float b = fmaf(-mean, a, be);
+        if (q >= lo && q < hi) {
+            const int cl = (8 * q) / HW;   // the chunk's channel in the group (HW % 8 == 0)
+            const float a = rstd * gsh[cl];
+            const float b = fmaf(-mean, a, bsh[cl]);
             float f[8];
             unpack8<ET>(xr[j], f);
 #pragma unroll
@@ -200,11 +215,15 @@ template <int ET>
 hipError_t launch_gn_e(const GroupNormArgs& a) {
     const long long n = (long long)(a.C / a.G) * a.HW;
     const unsigned grid = (unsigned)(a.B * a.G);
-    if (a.HW % 8 == 0 && n <= kGnResident) {
-        hipLaunchKernelGGL(gn_resident_kernel<ET>, dim3(grid), dim3(kGnThreads), 0,
-                           (hipStream_t)a.stream, (const uint16_t*)a.x, (const uint16_t*)a.gamma,
-                           (const uint16_t*)a.beta, (uint16_t*)a.y, a.C, (int)a.HW, a.G, (int)n,
-                           a.eps);
+    if (a.HW % 8 == 0 && n <= kGnResident && a.C / a.G <= kGnMaxCpg) {
+        // several workgroups per group when there are few groups, unless in place
+        const int ng = a.B * a.G;
+        const int S = (ng >= 256 || a.x == a.y) ? 1 : ng >= 128 ? 2 : 4;
+        const unsigned grid8 = (unsigned)((ng + 7) / 8 * 8 * S);
+        auto k = S == 1 ? gn_resident_kernel<ET, 1> : S == 2 ? gn_resident_kernel<ET, 2> : gn_resident_kernel<ET, 4>;
+        hipLaunchKernelGGL(k, dim3(grid8), dim3(kGnThreads), 0, (hipStream_t)a.stream,
+                           (const uint16_t*)a.x, (const uint16_t*)a.gamma, (const uint16_t*)a.beta,
+                           (uint16_t*)a.y, a.C, (int)a.HW, a.G, (int)n, a.eps, ng);
     } else {
         hipLaunchKernelGGL(gn_generic_kernel<ET>, dim3(grid), dim3(kGnThreads), 0,
                            (hipStream_t)a.stream, (const uint16_t*)a.x, (const uint16_t*)a.gamma,

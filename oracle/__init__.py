@@ -19,6 +19,8 @@ passages of the paper each function follows):
 * :func:`group_norm`, :func:`gelu` and :func:`geglu` -- the specialised
   kernels of Sec. 3.1: group normalisation (Eq. 1) and GELU (Eq. 2) with its
   split and multiply.
+* :func:`conv3x3` -- the 3x3 convolution (stride 1, zero padding 1) that
+  Sec. 3.3 computes with Winograd's algorithm, by its definition.
 
 Inputs are numpy arrays: float16, float32, float64, or bfloat16 passed as a
 uint16 bit-pattern array with ``dtype="bf16"``.
@@ -66,6 +68,8 @@ def _load():
         lib.oracle_gelu_f64.restype = i32
         lib.oracle_geglu_f64.argtypes = [vp, i32, i64, i32, i32, vp]
         lib.oracle_geglu_f64.restype = i32
+        lib.oracle_conv3x3_f64.argtypes = [vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, vp]
+        lib.oracle_conv3x3_f64.restype = i32
         lib.oracle_widen.argtypes = [vp, i32, i64, vp]
         lib.oracle_widen.restype = i32
         lib.oracle_num_threads.argtypes = [i32]
@@ -315,3 +319,27 @@ def geglu(h, dtype=None, nthreads=0):
     if _load().oracle_geglu_f64(_ptr(h), _code(h, dtype), M, F, int(nthreads), _ptr(out)) != 0:
         raise ValueError("oracle_geglu_f64 rejected its arguments")
     return out
+
+
+def conv3x3(x, w, bias=None, dtype=None, nthreads=0):
+    """3x3 convolution, stride 1, zero padding 1, in fp64: x [B, Ci, H, W],
+    w [Co, Ci, 3, 3], bias [Co] (x's type).  Returns [B, Co, H, W]."""
+    x, w = np.ascontiguousarray(x), np.ascontiguousarray(w)
+    if x.ndim != 4 or w.ndim != 4 or w.shape[1] != x.shape[1] or w.shape[2:] != (3, 3):
+        raise ValueError("expected x [B, Ci, H, W] and w [Co, Ci, 3, 3]")
+    if x.dtype != w.dtype:
+        raise TypeError("x and w must share one element type")
+    B, Ci, H, W = x.shape
+    Co = w.shape[0]
+    bp = None
+    if bias is not None:
+        bias = np.ascontiguousarray(bias)
+        if bias.shape != (Co,) or bias.dtype != x.dtype:
+            raise ValueError("bias must be [Co] of x's type")
+        bp = _ptr(bias)
+    y = np.empty((B, Co, H, W), dtype=np.float64)
+    rc = _load().oracle_conv3x3_f64(_ptr(x), _ptr(w), bp, _code(x, dtype), B, Ci, Co, H, W,
+                                    int(nthreads), _ptr(y))
+    if rc != 0:
+        raise ValueError("oracle_conv3x3_f64 rejected its arguments")
+    return y

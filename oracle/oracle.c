@@ -26,8 +26,9 @@
  * result does not depend on the thread count.
  *
  * Also the steps around the attention (the projections and the multi-head
- * block) and the specialised kernels of Sec. 3.1 (group normalisation, Eq. 1;
- * GELU, Eq. 2, with its split and multiply), each written out from its
+ * block), the specialised kernels of Sec. 3.1 (group normalisation, Eq. 1;
+ * GELU, Eq. 2, with its split and multiply) and the 3x3 convolution that
+ * Sec. 3.3 computes with Winograd's algorithm, each written out from its
  * definition below.
  *
  * Build: gcc -O2 -fopenmp -fPIC -shared (no -ffast-math).
@@ -523,6 +524,49 @@ int oracle_geglu_f64(const void *h, int dtype, int64_t M, int F, int nthreads, d
             const double a = or_elem(h, dtype, m * 2 * F + f);
             const double g = or_elem(h, dtype, m * 2 * F + F + f);
             out[m * F + f] = a * (0.5 * g * (1.0 + erf(g / sqrt(2.0))));
+        }
+    }
+    return 0;
+}
+
+/*
+ * 3x3 convolution, stride 1, zero padding 1 (the layers Sec. 3.3 accelerates
+ * with Winograd's algorithm; the oracle is the convolution's definition):
+ *   y[b][o][i][j] = bias[o] + sum_{c, u, v} w[o][c][u][v] * x[b][c][i + u - 1][j + v - 1]
+ * with x taken as 0 outside the H x W map.  x [B][Ci][H][W], w [Co][Ci][3][3],
+ * bias [Co] or NULL, all of type `dtype`; y [B][Co][H][W] doubles.
+ */
+int oracle_conv3x3_f64(const void *x, const void *w, const void *bias, int dtype, int B, int Ci,
+                       int Co, int H, int W, int nthreads, double *y)
+{
+    if (!x || !w || !y || B < 1 || Ci < 1 || Co < 1 || H < 1 || W < 1 || dtype < OR_F16 ||
+        dtype > OR_F64)
+        return 1;
+
+#pragma omp parallel for schedule(static) num_threads(oracle_num_threads(nthreads))
+    for (int64_t bo = 0; bo < (int64_t)B * Co; ++bo) {
+        const int64_t b = bo / Co;
+        const int o = (int)(bo % Co);
+        const double bo_v = bias ? or_elem(bias, dtype, o) : 0.0;
+        for (int i = 0; i < H; ++i) {
+            for (int j = 0; j < W; ++j) {
+                double acc = 0.0;
+                for (int c = 0; c < Ci; ++c) {
+                    for (int u = 0; u < 3; ++u) {
+                        const int ii = i + u - 1;
+                        if (ii < 0 || ii >= H)
+                            continue;
+                        for (int v = 0; v < 3; ++v) {
+                            const int jj = j + v - 1;
+                            if (jj < 0 || jj >= W)
+                                continue;
+                            acc += or_elem(w, dtype, (((int64_t)o * Ci + c) * 3 + u) * 3 + v) *
+                                   or_elem(x, dtype, ((b * Ci + c) * H + ii) * (int64_t)W + jj);
+                        }
+                    }
+                }
+                y[(bo * H + i) * (int64_t)W + j] = acc + bo_v;
+            }
         }
     }
     return 0;

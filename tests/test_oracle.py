@@ -651,3 +651,68 @@ def test_geglu_split_and_product():
     assert np.array_equal(oracle.geglu(v), oracle.gelu(v[:, 6:]))
     big = np.concatenate([rng.standard_normal((4, 6)), np.full((4, 6), 40.0)], axis=1)
     assert np.array_equal(oracle.geglu(big), big[:, :6] * 40.0)   # GELU(40) = 40 in fp64
+
+
+# ---- the 3x3 convolution of Sec. 3.3 (the oracle is its definition): pinned
+# against torch's fp64 conv2d, kernels with a known effect (a centred delta is
+# the identity, a corner delta shifts, which fails for a flipped kernel), the
+# zero padding (all-ones kernel on a constant map), and linearity.
+
+def test_conv3x3_matches_torch_fp64():
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(80)
+    for (B, Ci, Co, H, W) in ((2, 3, 4, 7, 9), (1, 1, 1, 1, 1), (1, 5, 2, 1, 6), (2, 8, 8, 4, 4)):
+        x = rng.standard_normal((B, Ci, H, W)).astype(np.float16)
+        w = (rng.standard_normal((Co, Ci, 3, 3)) / 3).astype(np.float16)
+        b = rng.standard_normal(Co).astype(np.float16)
+        y = oracle.conv3x3(x, w, b)
+        t = lambda a: torch.from_numpy(a.astype(np.float64))
+        ref = torch.nn.functional.conv2d(t(x), t(w), t(b), padding=1).numpy()
+        assert np.max(np.abs(y - ref)) <= 1e-13 * max(1.0, np.abs(ref).max()), (B, Ci, Co, H, W)
+
+
+def test_conv3x3_known_kernels():
+    rng = np.random.default_rng(81)
+    x = rng.standard_normal((2, 1, 5, 6)).astype(np.float16)
+    xd = x.astype(np.float64)
+    delta = np.zeros((1, 1, 3, 3), dtype=np.float16)
+    delta[0, 0, 1, 1] = 1
+    assert np.array_equal(oracle.conv3x3(x, delta), xd)
+    # w[.., 0, 0] = 1 reads the input one row up and one column left
+    corner = np.zeros((1, 1, 3, 3), dtype=np.float16)
+    corner[0, 0, 0, 0] = 1
+    want = np.zeros_like(xd)
+    want[..., 1:, 1:] = xd[..., :-1, :-1]
+    assert np.array_equal(oracle.conv3x3(x, corner), want)
+    # all-ones kernel on a constant map: 9c inside, 6c on the edges, 4c in the corners
+    c = np.full((1, 1, 4, 5), 2.0, dtype=np.float16)
+    y = oracle.conv3x3(c, np.ones((1, 1, 3, 3), dtype=np.float16))[0, 0]
+    assert np.array_equal(y[1:-1, 1:-1], np.full((2, 3), 18.0))
+    assert y[0, 0] == y[0, -1] == y[-1, 0] == y[-1, -1] == 8.0
+    assert np.array_equal(y[0, 1:-1], np.full(3, 12.0)) and np.array_equal(y[1:-1, 0], np.full(2, 12.0))
+
+
+def test_conv3x3_linearity_over_channels():
+    rng = np.random.default_rng(82)
+    x = rng.standard_normal((1, 2, 6, 5))
+    w = rng.standard_normal((3, 2, 3, 3))
+    both = oracle.conv3x3(x, w)
+    parts = oracle.conv3x3(x[:, :1], w[:, :1]) + oracle.conv3x3(x[:, 1:], w[:, 1:])
+    assert np.max(np.abs(both - parts)) <= 1e-13
+    assert np.max(np.abs(oracle.conv3x3(2.5 * x, w) - 2.5 * both)) <= 1e-12
+
+
+def test_winograd_table2_closed_forms():
+    """Table 2's figures follow from F(m x m, 3 x 3): an m x m output tile costs
+    (m + 2)^2 products instead of 9 m^2, the transformed input tile holds
+    (m + 2)^2 values for m^2 outputs, and a transformed 3x3 kernel (m + 2)^2
+    values for 9.  The paper prints them to two decimals (rounding up twice)."""
+    import os
+    path = os.path.join(os.path.dirname(__file__), "golden", "winograd_table2.txt")
+    rows = [list(map(float, l.split())) for l in open(path) if l.strip() and not l.startswith("#")]
+    assert [int(r[0]) for r in rows] == [2, 4, 6, 8]
+    for m, saving, tensor, weight in rows:
+        t = (m + 2) ** 2
+        assert abs(9 * m * m / t - saving) <= 0.005, m
+        assert abs(t / (m * m) - tensor) <= 0.025, m
+        assert abs(t / 9 - weight) <= 0.015, m

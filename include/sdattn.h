@@ -252,6 +252,36 @@ int sdattn_group_norm(const void *x, const void *gamma, const void *beta, void *
  */
 int sdattn_geglu(const void *h, void *out, long long M, int F, sdattn_dtype dtype, void *stream);
 
+/*
+ * 3x3 convolution, stride 1, zero padding 1, by Winograd's F(4x4, 3x3)
+ * algorithm (Sec. 3.3, the 4x4 tile of Table 2):
+ *   y[b, o, i, j] = bias[o] + sum_{c, u, v} w[o, c, u, v] x[b, c, i + u - 1, j + v - 1]
+ * on channel-major maps x [B, Ci, H, W] -> y [B, Co, H, W].
+ *
+ * sdattn_winograd_weights transforms the kernels w [Co, Ci, 3, 3] once per
+ * layer into u [36, Co, Ci] (sdattn_winograd_weights_elems(Co, Ci) elements,
+ * 4x the kernels, Table 2's weight factor; u 16-byte aligned).
+ * sdattn_conv3x3 then runs the input transform, 36 matrix products on the
+ * matrix cores and the output transform (three launches on `stream`) through
+ * a caller-owned workspace of sdattn_conv3x3_workspace(B, Ci, Co, H, W) bytes
+ * (the transformed input, 2.25x the input -- Table 2's tensor factor -- and
+ * the 36 products).  The transformed values are stored in `dtype` (fp16 or
+ * bf16) with fp32 arithmetic inside each step, so the error exceeds a direct
+ * convolution's by the transforms' growth (tested bound in the tests).
+ *
+ * Requirements: Ci and Co multiples of 8, at most 65536; H*W at most 2^26;
+ * x, u, y, workspace
+ * 16-byte aligned; bias [Co] of `dtype` or NULL; y must not overlap any input
+ * or the workspace, nor the workspace an input.
+ */
+long long sdattn_winograd_weights_elems(int Co, int Ci);
+int sdattn_winograd_weights(const void *w, void *u, int Co, int Ci, sdattn_dtype dtype,
+                            void *stream);
+long long sdattn_conv3x3_workspace(int B, int Ci, int Co, int H, int W);
+int sdattn_conv3x3(const void *x, const void *u, const void *bias, void *y, void *workspace,
+                   long long workspace_bytes, int B, int Ci, int Co, int H, int W,
+                   sdattn_dtype dtype, void *stream);
+
 /* Static English text for a status code (never NULL). */
 const char *sdattn_status_str(int status);
 

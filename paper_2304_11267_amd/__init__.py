@@ -9,6 +9,7 @@ falling back to anything else.
 from .binding import (  # noqa: F401
     SdattnError, forward, forward_ex, softmax_rows, logits, softmax_pv, linear,
     attention_block_workspace, attention_block, project_kv, attention_block_kv, group_norm, geglu,
+    winograd_weights, conv3x3_workspace, conv3x3,
     library_path,
     load_library,
     LAYOUT_ROWS, LAYOUT_HEADS,

@@ -29,7 +29,8 @@ DTYPE_F32 = 2
 EXPORTS = ("sdattn_forward", "sdattn_forward_ex", "sdattn_softmax_rows", "sdattn_logits",
            "sdattn_softmax_pv", "sdattn_linear", "sdattn_attention_block_workspace",
            "sdattn_attention_block", "sdattn_project_kv", "sdattn_attention_block_kv",
-           "sdattn_group_norm", "sdattn_geglu",
+           "sdattn_group_norm", "sdattn_geglu", "sdattn_winograd_weights_elems",
+           "sdattn_winograd_weights", "sdattn_conv3x3_workspace", "sdattn_conv3x3",
            "sdattn_status_str", "sdattn_last_hip_error", "sdattn_version")
 
 LAYOUT_ROWS = 0
@@ -86,6 +87,14 @@ def load_library():
     lib.sdattn_group_norm.restype = i32
     lib.sdattn_geglu.argtypes = [vp, vp, i64, i32, i32, vp]
     lib.sdattn_geglu.restype = i32
+    lib.sdattn_winograd_weights_elems.argtypes = [i32, i32]
+    lib.sdattn_winograd_weights_elems.restype = i64
+    lib.sdattn_winograd_weights.argtypes = [vp, vp, i32, i32, i32, vp]
+    lib.sdattn_winograd_weights.restype = i32
+    lib.sdattn_conv3x3_workspace.argtypes = [i32, i32, i32, i32, i32]
+    lib.sdattn_conv3x3_workspace.restype = i64
+    lib.sdattn_conv3x3.argtypes = [vp, vp, vp, vp, vp, i64, i32, i32, i32, i32, i32, i32, vp]
+    lib.sdattn_conv3x3.restype = i32
     lib.sdattn_status_str.argtypes = [i32]
     lib.sdattn_status_str.restype = ctypes.c_char_p
     lib.sdattn_last_hip_error.argtypes = []
@@ -335,3 +344,36 @@ def geglu(h, out, stream=None):
                                          _stream(stream))
     _check("sdattn_geglu", status)
     return out
+
+
+def winograd_weights(w, u, stream=None):
+    """u [36, Co, Ci] = the F(4x4, 3x3) transform of the kernels w [Co, Ci, 3, 3]."""
+    Co, Ci = w.shape[:2]
+    _expect(w, (Co, Ci, 3, 3), None, "w")
+    _expect(u, (36, Co, Ci), w, "u")
+    status = load_library().sdattn_winograd_weights(_dev(w, "w"), _dev(u, "u"), Co, Ci,
+                                                     _dtype_code(w), _stream(stream))
+    _check("sdattn_winograd_weights", status)
+    return u
+
+
+def conv3x3_workspace(B, Ci, Co, H, W):
+    """Bytes of workspace sdattn_conv3x3 needs."""
+    return int(load_library().sdattn_conv3x3_workspace(B, Ci, Co, H, W))
+
+
+def conv3x3(x, u, y, workspace, bias=None, stream=None):
+    """y [B, Co, H, W] = 3x3 convolution (stride 1, zero padding 1) of x [B, Ci, H, W]
+    with the transformed kernels u [36, Co, Ci] (from winograd_weights) + bias [Co]."""
+    B, Ci, H, W = x.shape
+    Co = u.shape[1]
+    _expect(u, (36, Co, Ci), x, "u")
+    _expect(y, (B, Co, H, W), x, "y")
+    if bias is not None:
+        _expect(bias, (Co,), x, "bias")
+    status = load_library().sdattn_conv3x3(
+        _dev(x, "x"), _dev(u, "u"), _dev(bias, "bias") if bias is not None else None, _dev(y, "y"),
+        _dev(workspace, "workspace"), workspace.numel() * workspace.element_size(),
+        B, Ci, Co, H, W, _dtype_code(x), _stream(stream))
+    _check("sdattn_conv3x3", status)
+    return y

@@ -18,7 +18,8 @@ LIB = os.path.join(HERE, "libsdattn.so")
 ARCH = "gfx950"
 
 SOURCES = ["attn_fwd.hip", "attn_fwd_short.hip", "attn_fwd_generic.hip", "softmax_rows.hip",
-           "twopass.hip", "linear.hip", "norm_act.hip", "sdattn_api.hip"]
+           "twopass.hip", "linear.hip", "norm_act.hip", "winograd.hip",
+           "sdattn_api.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 CFLAGS = [

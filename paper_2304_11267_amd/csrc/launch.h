@@ -76,6 +76,8 @@ struct LinearArgs {
     bool x_heads, y_heads;   // [B, H, L, C/H] instead of [B, L, C]
     int dtype;
     void* stream;
+    int batch = 1;           // independent products with the same sizes,
+    long long sx = 0, sw = 0, sy = 0;   // element strides between their x, w and y
 };
 long long linear_grid(int B, int L, int N);
 hipError_t launch_linear(const LinearArgs& a);
@@ -108,5 +110,28 @@ struct GegluArgs {
     void* stream;
 };
 hipError_t launch_geglu(const GegluArgs& a);
+
+// Winograd F(4x4, 3x3) convolution (winograd.hip).
+struct WinoFilterArgs {
+    const void* w;        // [Co, Ci, 3, 3]
+    void* u;              // [36, Co, Ci]
+    int Co, Ci;
+    int dtype;
+    void* stream;
+};
+struct WinoConvArgs {
+    const void* x;        // [B, Ci, H, W]
+    const void* u;        // [36, Co, Ci]
+    const void* bias;     // [Co] or null
+    void* y;              // [B, Co, H, W]
+    void* v;              // [36, T, Ci] workspace
+    void* m;              // [36, T, Co] workspace
+    int B, Ci, Co, H, W;
+    int dtype;
+    void* stream;
+};
+long long wino_tiles(int B, int H, int W);
+hipError_t launch_wino_filter(const WinoFilterArgs& a);
+hipError_t launch_wino_conv(const WinoConvArgs& a);
 
 }  // namespace sdattn

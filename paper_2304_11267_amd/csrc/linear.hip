@@ -9,9 +9,11 @@
 // the output projection -- neither needs a transpose of its own.
 //
 // One launch may carry up to three independent products (the block's Q, K
-// and V projections, whose inputs differ for cross-attention); each
-// workgroup finds its product from its tile index, so the small context
-// projections run beside the large latent one instead of after it.
+// and V projections, whose inputs differ for cross-attention), each possibly
+// a batch of equal-sized products at fixed strides (the 36 products of a
+// Winograd convolution); each workgroup finds its product and batch item
+// from its tile index, so the small context projections run beside the
+// large latent one instead of after it.
 //
 // Workgroup tile: 128 token rows x 64 output channels, four waves of 32 rows.
 // Each 64-channel slice of the x and w tiles is copied global -> LDS with
@@ -50,6 +52,8 @@ struct LinProblem {
     int M, K, N, L;         // M = B*L token rows
     int xhw, yhw;           // head widths of the heads layouts (1 for rows layout)
     int nnt, tile0;         // channel tiles; first tile index of this product
+    int per_batch;          // tiles of one batch item
+    long long sx, sw, sy;   // element strides between batch items
 };
 struct LinGroup {
     LinProblem p[kMaxLinearProblems];
@@ -122,10 +126,11 @@ __global__ __launch_bounds__(256) void linear_kernel(const LinGroup grp) {
     const int tile = xcd_remap(blockIdx.x, gridDim.x);
     const int pi = (grp.n > 2 && tile >= grp.p[2].tile0) ? 2 : (grp.n > 1 && tile >= grp.p[1].tile0) ? 1 : 0;
     const LinProblem& P = grp.p[pi];
-    const uint16_t* __restrict__ X = P.x;
-    const uint16_t* __restrict__ W = P.w;
+    const int bi = (tile - P.tile0) / P.per_batch;     // batch item
+    const int local = tile - P.tile0 - bi * P.per_batch;
+    const uint16_t* __restrict__ X = P.x + bi * P.sx;
+    const uint16_t* __restrict__ W = P.w + bi * P.sw;
     const int M = P.M, K = P.K, N = P.N, L = P.L, xhw = P.xhw;
-    const int local = tile - P.tile0;
     const int nt = local % P.nnt;        // consecutive workgroups share the token rows
     const int m0 = (local / P.nnt) * kBM;
     const int n0 = nt * kBN;
@@ -271,7 +276,7 @@ __global__ __launch_bounds__(256) void linear_kernel(const LinGroup grp) {
     const int r0 = threadIdx.x >> 3;
     if (n < N) {
         const int yhw = P.yhw;
-        uint16_t* __restrict__ Yc = P.y + chan_offset<YH>(n, L, yhw, 1.0f / (float)yhw);
+        uint16_t* __restrict__ Yc = P.y + bi * P.sy + chan_offset<YH>(n, L, yhw, 1.0f / (float)yhw);
         int b = (m0 + r0) / L, l = (m0 + r0) - b * L;   // token row m = b*L + l
 #pragma unroll
         for (int j = 0; j < kBM * kBN / 8 / 256; ++j) {
@@ -336,7 +341,13 @@ hipError_t launch_linear_group(const LinearArgs* a, int n) {
         p.yhw = a[i].y_heads ? a[i].N / a[i].H : 1;
         p.nnt = (a[i].N + kBN - 1) / kBN;
         p.tile0 = (int)nblk;
-        nblk += tiles_of(a[i]);
+        p.per_batch = (int)tiles_of(a[i]);
+        p.sx = a[i].sx;
+        p.sw = a[i].sw;
+        p.sy = a[i].sy;
+        if (a[i].batch < 1) return hipErrorInvalidValue;
+        nblk += tiles_of(a[i]) * a[i].batch;
+        if (nblk > 0x7fffffff) return hipErrorInvalidValue;
     }
     g.n = n;
     if (nblk > 0x7fffffff) return hipErrorInvalidValue;

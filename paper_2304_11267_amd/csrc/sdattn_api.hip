@@ -373,6 +373,65 @@ int sdattn_geglu(const void* h, void* out, long long M, int F, sdattn_dtype dtyp
     return finish(sdattn::launch_geglu(a));
 }
 
+long long sdattn_winograd_weights_elems(int Co, int Ci) {
+    const long long n = checked_mul({36, Co, Ci});
+    return n < 0 ? -1 : n;
+}
+
+int sdattn_winograd_weights(const void* w, void* u, int Co, int Ci, sdattn_dtype dtype,
+                            void* stream) {
+    if (!w || !u) return SDATTN_ERR_INVALID_ARG;
+    if (Co < 1 || Ci < 1) return SDATTN_ERR_INVALID_ARG;
+    if (dtype != SDATTN_F16 && dtype != SDATTN_BF16)
+        return dtype == SDATTN_F32 ? SDATTN_ERR_UNSUPPORTED : SDATTN_ERR_INVALID_ARG;
+    const long long nu = sdattn_winograd_weights_elems(Co, Ci);
+    if (nu < 0) return SDATTN_ERR_UNSUPPORTED;
+    if (!aligned(w, 2) || !aligned(u, 16)) return SDATTN_ERR_MISALIGNED;
+    if (overlap(u, 2ULL * nu, w, 2ULL * 9 * Co * Ci)) return SDATTN_ERR_INVALID_ARG;
+    (void)hipGetLastError();
+    sdattn::WinoFilterArgs a{w, u, Co, Ci, (int)dtype, stream};
+    return finish(sdattn::launch_wino_filter(a));
+}
+
+// V [36][T][Ci] and M [36][T][Co], each rounded up to 256 bytes
+long long sdattn_conv3x3_workspace(int B, int Ci, int Co, int H, int W) {
+    if (B < 1 || Ci < 1 || Co < 1 || H < 1 || W < 1) return -1;
+    const long long T = sdattn::wino_tiles(B, H, W);
+    const long long nv = checked_mul({36, T, Ci}), nm = checked_mul({36, T, Co});
+    if (nv < 0 || nm < 0) return -1;
+    return block_part(nv) + block_part(nm);
+}
+
+int sdattn_conv3x3(const void* x, const void* u, const void* bias, void* y, void* workspace,
+                   long long workspace_bytes, int B, int Ci, int Co, int H, int W,
+                   sdattn_dtype dtype, void* stream) {
+    if (!x || !u || !y || !workspace) return SDATTN_ERR_INVALID_ARG;
+    if (B < 1 || Ci < 1 || Co < 1 || H < 1 || W < 1) return SDATTN_ERR_INVALID_ARG;
+    if (dtype != SDATTN_F16 && dtype != SDATTN_BF16)
+        return dtype == SDATTN_F32 ? SDATTN_ERR_UNSUPPORTED : SDATTN_ERR_INVALID_ARG;
+    if (Ci % 8 != 0 || Co % 8 != 0 || Ci > 65536 || Co > 65536) return SDATTN_ERR_UNSUPPORTED;
+    const long long nx = checked_mul({B, Ci, H, W}), ny = checked_mul({B, Co, H, W});
+    const long long need = sdattn_conv3x3_workspace(B, Ci, Co, H, W);
+    const long long T = sdattn::wino_tiles(B, H, W);
+    // the input transform addresses 32 channel planes of one image in 32 bits
+    if (nx < 0 || ny < 0 || need < 0 || T > INT_MAX / 2 || (long long)H * W > (1LL << 26) ||
+        (long long)B * ((H + 3) / 4) * ((W + 63) / 64) > INT_MAX)
+        return SDATTN_ERR_UNSUPPORTED;
+    if (workspace_bytes < need) return SDATTN_ERR_INVALID_ARG;
+    if (!aligned(x, 16) || !aligned(u, 16) || !aligned(y, 16) || !aligned(workspace, 16) ||
+        (bias && !aligned(bias, 2)))
+        return SDATTN_ERR_MISALIGNED;
+    const unsigned long long yb = 2ULL * ny, ub = 2ULL * 36 * Co * Ci, wb = (unsigned long long)need;
+    if (overlap(y, yb, x, 2ULL * nx) || overlap(y, yb, u, ub) || overlap(y, yb, workspace, wb) ||
+        (bias && overlap(y, yb, bias, 2ULL * Co)) || overlap(workspace, wb, x, 2ULL * nx) ||
+        overlap(workspace, wb, u, ub) || (bias && overlap(workspace, wb, bias, 2ULL * Co)))
+        return SDATTN_ERR_INVALID_ARG;
+    (void)hipGetLastError();
+    void* m = (char*)workspace + block_part(36 * T * Ci);
+    sdattn::WinoConvArgs a{x, u, bias, y, workspace, m, B, Ci, Co, H, W, (int)dtype, stream};
+    return finish(sdattn::launch_wino_conv(a));
+}
+
 const char* sdattn_status_str(int status) {
     switch (status) {
         case SDATTN_OK: return "ok";

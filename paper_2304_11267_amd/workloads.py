@@ -300,3 +300,17 @@ def make_geglu(M, F, seed, dtype="f16", sigma=1.5):
 
 def geglu_inputs(case: GegluCase, dtype="f16"):
     return make_geglu(case.M, case.F, case.seed, dtype)
+
+
+# The UNet's 3x3 convolutions (Sec. 3.3): C -> C channels at each latent level.
+CONV_LEVELS = {64: 320, 32: 640, 16: 1280, 8: 1280}
+
+
+def make_conv(B, Ci, Co, H, W, seed, dtype="f16"):
+    """x [B, Ci, H, W] ~ N(0, 1), w [Co, Ci, 3, 3] ~ N(0, 1/(9 Ci)), bias ~ N(0, 0.1^2),
+    drawn in that order from default_rng(seed) in float32."""
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((B, Ci, H, W), dtype=np.float32)
+    w = rng.standard_normal((Co, Ci, 3, 3), dtype=np.float32) / np.float32(np.sqrt(9 * Ci))
+    b = rng.standard_normal(Co, dtype=np.float32) * np.float32(0.1)
+    return tuple(_cast(t, dtype) for t in (x, w, b))

@@ -294,3 +294,43 @@ def test_geglu_checks(lib):
     assert ge(dtype=F32) == UNSUPPORTED
     assert ge(out=ctypes.c_void_p(0x40000004)) == MISALIGNED
     assert ge(out=ctypes.c_void_p(0x10000000 + 2 * 1280 * 2)) == INVALID   # out inside h
+
+
+def test_winograd_checks_and_table2_factors(lib):
+    import os
+    # Table 2, 4x4 tile: weights grow 4x, the transformed input 2.25x
+    path = os.path.join(os.path.dirname(__file__), "golden", "winograd_table2.txt")
+    row = [list(map(float, l.split())) for l in open(path) if l.strip() and not l.startswith("#")][1]
+    assert row[0] == 4
+    assert lib.sdattn_winograd_weights_elems(320, 640) == row[3] * 9 * 320 * 640
+    B, Ci, Co, H, W = 2, 320, 640, 64, 64
+    part = lambda e: (2 * e + 255) // 256 * 256
+    T = B * (H // 4) * (W // 4)
+    ws = lib.sdattn_conv3x3_workspace(B, Ci, Co, H, W)
+    assert ws == part(36 * T * Ci) + part(36 * T * Co)
+    assert 36 * T * Ci == row[2] * B * Ci * H * W
+    assert lib.sdattn_conv3x3_workspace(0, Ci, Co, H, W) == -1
+
+    U = ctypes.c_void_p(0x60000000)
+
+    def wt(w=KA, u=U, Co=64, Ci=32, dtype=F16):
+        return lib.sdattn_winograd_weights(w, u, Co, Ci, dtype, None)
+    assert wt(w=None) == INVALID and wt(u=None) == INVALID and wt(Co=0) == INVALID
+    assert wt(dtype=F32) == UNSUPPORTED
+    assert wt(u=ctypes.c_void_p(0x60000008)) == MISALIGNED
+    assert wt(u=ctypes.c_void_p(0x20000000 + 64)) == INVALID     # u overlaps w
+
+    def cv(x=QA, u=U, bias=VA, y=OA, ws=ctypes.c_void_p(0x50000000), wsb=1 << 24, B=1, Ci=32,
+           Co=64, H=16, W=16, dtype=F16):
+        return lib.sdattn_conv3x3(x, u, bias, y, ws, wsb, B, Ci, Co, H, W, dtype, None)
+    for field in ("x", "u", "y", "ws"):
+        assert cv(**{field: None}) == INVALID
+    for field in ("B", "Ci", "Co", "H", "W"):
+        assert cv(**{field: 0}) == INVALID
+    assert cv(Ci=36) == UNSUPPORTED                     # Ci % 8
+    assert cv(Co=20) == UNSUPPORTED                     # Co % 8
+    assert cv(dtype=F32) == UNSUPPORTED
+    assert cv(wsb=lib.sdattn_conv3x3_workspace(1, 32, 64, 16, 16) - 1) == INVALID
+    assert cv(x=ctypes.c_void_p(0x10000008)) == MISALIGNED
+    assert cv(y=ctypes.c_void_p(0x10000000 + 256)) == INVALID      # y overlaps x
+    assert cv(ws=ctypes.c_void_p(0x60000000 + 512)) == INVALID     # workspace overlaps u

@@ -269,7 +269,7 @@ int sdattn_geglu(const void *h, void *out, long long M, int F, sdattn_dtype dtyp
  * bf16) with fp32 arithmetic inside each step, so the error exceeds a direct
  * convolution's by the transforms' growth (tested bound in the tests).
  *
- * Requirements: Ci and Co multiples of 8, at most 65536; H*W at most 2^26;
+ * Requirements: Ci and Co multiples of 8, at most 65536; H*W at most 2^25;
  * x, u, y, workspace
  * 16-byte aligned; bias [Co] of `dtype` or NULL; y must not overlap any input
  * or the workspace, nor the workspace an input.

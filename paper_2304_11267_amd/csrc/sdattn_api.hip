@@ -413,9 +413,9 @@ int sdattn_conv3x3(const void* x, const void* u, const void* bias, void* y, void
     const long long nx = checked_mul({B, Ci, H, W}), ny = checked_mul({B, Co, H, W});
     const long long need = sdattn_conv3x3_workspace(B, Ci, Co, H, W);
     const long long T = sdattn::wino_tiles(B, H, W);
-    // the input transform addresses 32 channel planes of one image in 32 bits
-    if (nx < 0 || ny < 0 || need < 0 || T > INT_MAX / 2 || (long long)H * W > (1LL << 26) ||
-        (long long)B * ((H + 3) / 4) * ((W + 63) / 64) > INT_MAX)
+    // the input transform addresses 64 channel planes of one image in 32 bits
+    if (nx < 0 || ny < 0 || need < 0 || T > INT_MAX / 2 || (long long)H * W > (1LL << 25) ||
+        (long long)B * ((H + 3) / 4) * ((W + 31) / 32) > INT_MAX)
         return SDATTN_ERR_UNSUPPORTED;
     if (workspace_bytes < need) return SDATTN_ERR_INVALID_ARG;
     if (!aligned(x, 16) || !aligned(u, 16) || !aligned(y, 16) || !aligned(workspace, 16) ||

@@ -44,10 +44,15 @@ __device__ constexpr float kAT[4][6] = {{1, 1, 1, 1, 1, 0},
                                         {0, 1, 1, 0.25f, 4, 0},
                                         {0, 1, -1, 0.125f, -8, 1}};
 
-constexpr int kTilesPerWg = 16;   // a segment of 16 tiles along a tile row (64 pixels)
-constexpr int kChanPerWg = 32;    // channels per workgroup in the input / output transforms
-constexpr int kPatchCols = 72;    // input columns staged per segment: 4*tx0 - 4 .. 4*tx0 + 67
-constexpr int kPlane = 6 * kPatchCols + 8;   // halves per channel plane in LDS (padded)
+// input transform: 8 tiles of a tile row x 64 channels per workgroup (the V
+// stores of a tile are then whole 128-byte lines)
+constexpr int kInTiles = 8;
+constexpr int kInChan = 64;
+constexpr int kPatchCols = 4 * kInTiles + 8;   // input columns staged: 4*tx0 - 4 .. 4*tx0 + 35
+constexpr int kPlane = 6 * kPatchCols + 8;     // halves per channel plane in LDS (padded)
+// output transform: 16 tiles (64 pixels, whole output rows of 128 bytes) x 32 channels
+constexpr int kTilesPerWg = 16;
+constexpr int kChanPerWg = 32;
 
 // 1. U[xi][o][c] = (G g G^T)[xi], one thread per (o, c).
 template <int ET>
@@ -73,31 +78,32 @@ __global__ __launch_bounds__(256) void wino_filter_kernel(const uint16_t* __rest
                 from_float<ET>(t[i][0] * kG[j][0] + t[i][1] * kG[j][1] + t[i][2] * kG[j][2]);
 }
 
-// 2. V[xi][t][c] = (B^T d B)[xi].  A workgroup takes 16 tiles of one tile row
-// and 32 channels: the 6 x 72 input window of each channel goes to LDS (8-byte
-// loads when W % 4 == 0), then each thread transforms two (tile, channel)
-// patches and writes 36 values, consecutive lanes on consecutive channels.
+// 2. V[xi][t][c] = (B^T d B)[xi].  A workgroup takes 8 tiles of one tile row
+// and 64 channels: the 6 x 40 input window of each channel goes to LDS (8-byte
+// loads when W % 4 == 0), then each thread transforms the patches of one tile
+// in two consecutive channels and writes 36 channel pairs, consecutive lanes
+// on consecutive pairs.
 template <int ET>
 __global__ __launch_bounds__(256) void wino_input_kernel(const uint16_t* __restrict__ X,
                                                          uint16_t* __restrict__ V, int Ci, int H,
                                                          int W, int th, int tw, int nseg, int T) {
-    __shared__ uint16_t patch[kChanPerWg * kPlane];
-    const int cb = blockIdx.y * kChanPerWg;
+    __shared__ uint16_t patch[kInChan * kPlane];
+    const int cb = blockIdx.y * kInChan;
     const int seg = blockIdx.x % nseg;
     const int brow = blockIdx.x / nseg;        // b * th + ty
     const int b = brow / th, ty = brow - b * th;
-    const int tx0 = seg * kTilesPerWg;
+    const int tx0 = seg * kInTiles;
     const int r0 = 4 * ty - 1, c0 = 4 * tx0 - 4;
     const int tid = threadIdx.x;
 
     // this workgroup's channel planes; offsets inside them fit in 32 bits
     const uint16_t* xb = X + ((size_t)b * Ci + cb) * H * W;
-    const int nch = min(kChanPerWg, Ci - cb);
+    const int nch = min(kInChan, Ci - cb);
     if (W % 4 == 0) {
         // 32 channels x 6 rows x 18 chunks of 4 columns: every load issued
         // before the first LDS write, so their latencies overlap
         constexpr int kRowChunks = kPatchCols / 4;
-        constexpr int kChunks = kChanPerWg * 6 * kRowChunks;
+        constexpr int kChunks = kInChan * 6 * kRowChunks;
         constexpr int kPer = (kChunks + 255) / 256;
         u32x2 v[kPer];
 #pragma unroll
@@ -118,7 +124,7 @@ __global__ __launch_bounds__(256) void wino_input_kernel(const uint16_t* __restr
         }
     } else {
 #pragma unroll 1
-        for (int q = tid; q < kChanPerWg * 6 * kPatchCols; q += 256) {
+        for (int q = tid; q < kInChan * 6 * kPatchCols; q += 256) {
             const int row = q / kPatchCols, cc = q - row * kPatchCols;
             const int ch = row / 6, r = row - ch * 6;
             const int gr = r0 + r, gc = c0 + cc;
@@ -128,47 +134,61 @@ __global__ __launch_bounds__(256) void wino_input_kernel(const uint16_t* __restr
     }
     __syncthreads();
 
-#pragma unroll 1
-    for (int k = 0; k < kTilesPerWg * kChanPerWg / 256; ++k) {
-        const int p = tid + 256 * k;
-        const int ch = p % kChanPerWg, t = p / kChanPerWg;
-        if (tx0 + t >= tw || cb + ch >= Ci) continue;
-        const uint16_t* src = patch + ch * kPlane + 4 * t + 3;   // global column 4*(tx0 + t) - 1
-        float d[6][6];
+    // one tile and two consecutive channels per thread (Ci % 8 == 0, so both
+    // exist together): 4-byte stores of the channel pair
+    static_assert(kInTiles * kInChan / 2 == 256, "one (tile, channel pair) per thread");
+    {
+        const int cp = tid % (kInChan / 2), t = tid / (kInChan / 2);
+        const int ch = 2 * cp;
+        if (tx0 + t < tw && cb + ch < Ci) {
+            const uint16_t* src = patch + ch * kPlane + 4 * t + 3;   // global column 4*(tx0 + t) - 1
+            float d0[6][6], d1[6][6];
 #pragma unroll
-        for (int i = 0; i < 6; ++i)
+            for (int i = 0; i < 6; ++i)
 #pragma unroll
-            for (int j = 0; j < 6; ++j) d[i][j] = to_float<ET>(src[i * kPatchCols + j]);
-        const size_t tg = (size_t)brow * tw + tx0 + t;   // tile index (b*th + ty)*tw + tx
-        const size_t stride = (size_t)T * Ci;
-        uint16_t* vo = V + tg * Ci + cb + ch;
-        // one row of B^T d at a time, then that row of (B^T d) B
+                for (int j = 0; j < 6; ++j) {
+                    d0[i][j] = to_float<ET>(src[i * kPatchCols + j]);
+                    d1[i][j] = to_float<ET>(src[kPlane + i * kPatchCols + j]);
+                }
+            const size_t tg = (size_t)brow * tw + tx0 + t;   // tile index (b*th + ty)*tw + tx
+            const size_t stride = (size_t)T * Ci;
+            uint16_t* vo = V + tg * Ci + cb + ch;
+            // one row of B^T d at a time, then that row of (B^T d) B
 #pragma unroll
-        for (int i = 0; i < 6; ++i) {
-            float s[6];
+            for (int i = 0; i < 6; ++i) {
+                float s0[6], s1[6];
 #pragma unroll
-            for (int j = 0; j < 6; ++j) {
-                float a = 0.0f;
+                for (int j = 0; j < 6; ++j) {
+                    float a0 = 0.0f, a1 = 0.0f;
 #pragma unroll
-                for (int r = 0; r < 6; ++r)
-                    if (kBT[i][r] != 0.0f) a += kBT[i][r] * d[r][j];
-                s[j] = a;
-            }
+                    for (int r = 0; r < 6; ++r)
+                        if (kBT[i][r] != 0.0f) {
+                            a0 += kBT[i][r] * d0[r][j];
+                            a1 += kBT[i][r] * d1[r][j];
+                        }
+                    s0[j] = a0;
+                    s1[j] = a1;
+                }
 #pragma unroll
-            for (int j = 0; j < 6; ++j) {
-                float a = 0.0f;
+                for (int j = 0; j < 6; ++j) {
+                    float a0 = 0.0f, a1 = 0.0f;
 #pragma unroll
-                for (int r = 0; r < 6; ++r)
-                    if (kBT[j][r] != 0.0f) a += s[r] * kBT[j][r];
-                vo[(6 * i + j) * stride] = from_float<ET>(a);
+                    for (int r = 0; r < 6; ++r)
+                        if (kBT[j][r] != 0.0f) {
+                            a0 += s0[r] * kBT[j][r];
+                            a1 += s1[r] * kBT[j][r];
+                        }
+                    *(uint32_t*)(vo + (6 * i + j) * stride) = pack2<ET>(a0, a1);
+                }
             }
         }
     }
 }
 
 // 4. y = A^T M A + bias.  A workgroup takes 16 tiles of one tile row and 32
-// output channels; each thread transforms two (tile, channel) pairs into LDS,
-// then the 4 x 64 output window of each channel is written row by row.
+// output channels; each thread transforms one tile of two consecutive output
+// channels into LDS, then the 4 x 64 output window of each channel is written
+// row by row.
 template <int ET>
 __global__ __launch_bounds__(256) void wino_output_kernel(const uint16_t* __restrict__ Mt,
                                                           const uint16_t* __restrict__ Bias,
@@ -182,40 +202,54 @@ __global__ __launch_bounds__(256) void wino_output_kernel(const uint16_t* __rest
     const int tx0 = seg * kTilesPerWg;
     const int tid = threadIdx.x;
 
-#pragma unroll 1
-    for (int k = 0; k < kTilesPerWg * kChanPerWg / 256; ++k) {
-        const int p = tid + 256 * k;
-        const int ch = p % kChanPerWg, t = p / kChanPerWg;
-        if (tx0 + t >= tw || ob + ch >= Co) continue;
-        const size_t tg = (size_t)brow * tw + tx0 + t;
-        const size_t stride = (size_t)T * Co;
-        float m[6][6];
+    {
+        // one tile and two consecutive output channels per thread (Co % 8 == 0)
+        const int cp = tid % (kChanPerWg / 2), t = tid / (kChanPerWg / 2);
+        const int ch = 2 * cp;
+        if (tx0 + t < tw && ob + ch < Co) {
+            const size_t tg = (size_t)brow * tw + tx0 + t;
+            const size_t stride = (size_t)T * Co;
+            const uint16_t* mi = Mt + tg * Co + ob + ch;
+            float m0[6][6], m1[6][6];
 #pragma unroll
-        for (int i = 0; i < 6; ++i)
+            for (int i = 0; i < 6; ++i)
 #pragma unroll
-            for (int j = 0; j < 6; ++j) m[i][j] = to_float<ET>(Mt[(6 * i + j) * stride + tg * Co + ob + ch]);
-        float s[4][6];   // A^T m
+                for (int j = 0; j < 6; ++j) {
+                    const uint32_t w = *(const uint32_t*)(mi + (6 * i + j) * stride);
+                    m0[i][j] = to_float<ET>((uint16_t)(w & 0xffffu));
+                    m1[i][j] = to_float<ET>((uint16_t)(w >> 16));
+                }
+            const float bias0 = Bias ? to_float<ET>(Bias[ob + ch]) : 0.0f;
+            const float bias1 = Bias ? to_float<ET>(Bias[ob + ch + 1]) : 0.0f;
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < 4; ++i) {
+                float s0[6], s1[6];   // row i of A^T m
 #pragma unroll
-            for (int j = 0; j < 6; ++j) {
-                float a = 0.0f;
+                for (int j = 0; j < 6; ++j) {
+                    float a0 = 0.0f, a1 = 0.0f;
 #pragma unroll
-                for (int r = 0; r < 6; ++r)
-                    if (kAT[i][r] != 0.0f) a += kAT[i][r] * m[r][j];
-                s[i][j] = a;
+                    for (int r = 0; r < 6; ++r)
+                        if (kAT[i][r] != 0.0f) {
+                            a0 += kAT[i][r] * m0[r][j];
+                            a1 += kAT[i][r] * m1[r][j];
+                        }
+                    s0[j] = a0;
+                    s1[j] = a1;
+                }
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    float a0 = bias0, a1 = bias1;
+#pragma unroll
+                    for (int r = 0; r < 6; ++r)
+                        if (kAT[j][r] != 0.0f) {
+                            a0 += s0[r] * kAT[j][r];
+                            a1 += s1[r] * kAT[j][r];
+                        }
+                    out[(ch * 4 + i) * 64 + 4 * t + j] = from_float<ET>(a0);
+                    out[((ch + 1) * 4 + i) * 64 + 4 * t + j] = from_float<ET>(a1);
+                }
             }
-        const float bias = Bias ? to_float<ET>(Bias[ob + ch]) : 0.0f;
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                float a = bias;
-#pragma unroll
-                for (int r = 0; r < 6; ++r)
-                    if (kAT[j][r] != 0.0f) a += s[i][r] * kAT[j][r];
-                out[(ch * 4 + i) * 64 + 4 * t + j] = from_float<ET>(a);
-            }
+        }
     }
     __syncthreads();
 
@@ -253,13 +287,14 @@ template <int ET>
 hipError_t launch_conv_e(const WinoConvArgs& a) {
     const int th = (a.H + 3) / 4, tw = (a.W + 3) / 4;
     const int nseg = (tw + kTilesPerWg - 1) / kTilesPerWg;
+    const int nseg_in = (tw + kInTiles - 1) / kInTiles;
     const long long T = (long long)a.B * th * tw;
     uint16_t* V = (uint16_t*)a.v;
     uint16_t* M = (uint16_t*)a.m;
     hipStream_t s = (hipStream_t)a.stream;
-    const dim3 gin((unsigned)(a.B * th * nseg), (unsigned)((a.Ci + kChanPerWg - 1) / kChanPerWg));
+    const dim3 gin((unsigned)(a.B * th * nseg_in), (unsigned)((a.Ci + kInChan - 1) / kInChan));
     hipLaunchKernelGGL(wino_input_kernel<ET>, gin, dim3(256), 0, s, (const uint16_t*)a.x, V, a.Ci,
-                       a.H, a.W, th, tw, nseg, (int)T);
+                       a.H, a.W, th, tw, nseg_in, (int)T);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     // 36 products M[xi] = V[xi] U[xi]^T: tiles are the rows, input channels the

@@ -160,6 +160,7 @@ def main():
         out["attention_block"] = bench_block(torch, sd, wl, dev, stream,
                                              {"self": self_ms, "cross": warm_ms})
         out["norm_act"] = bench_norm_act(torch, sd, wl, dev, stream)
+        out["conv3x3_winograd"] = bench_conv(torch, sd, wl, dev, stream)
 
     if args.copy_calibration:
         out["copy_calibration"] = copy_calibration(torch, dev, stream)
@@ -360,6 +361,47 @@ def bench_norm_act(torch, sd, wl, dev, stream, launches=50, reps=3):
         res[name] = {"us": round(ms * 1e3, 2), "bytes": nbytes, "gbs": round(gbs, 1),
                      "frac_hbm": round(gbs / PEAK_HBM_GBS, 4), "shape": shape}
     return res
+
+
+def bench_conv(torch, sd, wl, dev, stream, launches=30, reps=3):
+    """The UNet's 3x3 convolution at the 64x64 level (2 x 320 x 64 x 64 -> 320
+    channels) by Winograd F(4x4, 3x3), launched back to back behind a busy GPU;
+    the kernel transform (once per layer) is timed separately.  Also the same
+    convolution through torch.nn.functional.conv2d (MIOpen) for reference."""
+
+    def timed(call):
+        call()
+        torch.cuda.synchronize()
+        best = None
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda._sleep(20_000_000)
+            e0.record(stream)
+            for _ in range(launches):
+                call()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / launches
+            best = ms if best is None else min(best, ms)
+        return best
+
+    B, C, L = 2, wl.CONV_LEVELS[64], 64
+    x, w, b = (torch.from_numpy(t).to(dev) for t in wl.make_conv(B, C, C, L, L, wl.SEED0 + 51))
+    u = torch.empty(36, C, C, dtype=x.dtype, device=dev)
+    ws = torch.empty(sd.conv3x3_workspace(B, C, C, L, L), dtype=torch.uint8, device=dev)
+    y = torch.empty(B, C, L, L, dtype=x.dtype, device=dev)
+    wt_ms = timed(lambda: sd.winograd_weights(w, u, stream))
+    ms = timed(lambda: sd.conv3x3(x, u, y, ws, b, stream))
+    ref_ms = timed(lambda: torch.nn.functional.conv2d(x, w, b, padding=1))
+    direct = 2 * 9 * C * C * L * L * B
+    tiles = B * (L // 4) * (L // 4)
+    wino = 2 * 36 * tiles * C * C
+    return {"us": round(ms * 1e3, 2), "direct_equivalent_tflops": round(direct / (ms * 1e-3) / 1e12, 1),
+            "winograd_product_tflops": round(wino / (ms * 1e-3) / 1e12, 1),
+            "direct_flops": direct, "winograd_product_flops": wino,
+            "weight_transform_us": round(wt_ms * 1e3, 2),
+            "torch_conv2d_us": round(ref_ms * 1e3, 2),
+            "shape": f"x [{B},{C},{L},{L}] w [{C},{C},3,3]"}
 
 
 def copy_calibration(torch, dev, stream, nbytes=256 << 20, reps=3):

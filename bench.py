@@ -43,7 +43,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing")
     ap.add_argument("--no-extras", action="store_true",
                     help="time only the step (no cold cross or softmax_rows legs)")
-    ap.add_argument("--cpu-rows-per-head", type=int, default=2560,
+    ap.add_argument("--cpu-rows-per-head", type=int, default=5120,
                     help="self-attention rows per (b, h) the oracle times")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 256 MiB device copy (scales the HBM traffic counters)")

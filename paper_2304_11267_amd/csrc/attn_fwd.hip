@@ -203,6 +203,41 @@ __global__ __launch_bounds__(Geom<D>::kThreads, Geom<D>::kWavesPerSimd) void att
             qreg[j][s] = v;
         }
 
+    // The shift folded into Q K^T (fp16, no statistics, D % 16 == 8): Q is
+    // scaled by c once, and the spare k slot d = D of the last k-step holds
+    // -m in Q against a constant 1 in K, so the MFMA returns c s - m and the
+    // exponent needs no per-score FMA.  m is rounded to fp16 first; any
+    // reference value works, as long as every key of the row uses the same.
+    constexpr bool kFold = ET == kF16 && !STATS && D % 16 == 8;
+    if constexpr (kFold) {
+#pragma unroll
+        for (int j = 0; j < QB; ++j)
+#pragma unroll
+            for (int s = 0; s < DK; ++s)
+#pragma unroll
+                for (int w = 0; w < 4; ++w) {
+                    const uint32_t x = qreg[j][s][w];
+                    qreg[j][s][w] = pack2<ET>(to_float<ET>((uint16_t)(x & 0xffffu)) * c,
+                                              to_float<ET>((uint16_t)(x >> 16)) * c);
+                }
+    }
+    // K operand of the last k-step for the lanes holding d = D .. D + 7: a 1
+    // at d = D, zeros after (used only when kFold)
+    const u32x4 kone = {(uint32_t)from_float<ET>(1.0f), 0u, 0u, 0u};
+    auto k_last = [&](u32x4 a) __attribute__((always_inline)) -> u32x4 {
+        if constexpr (kFold) return half ? kone : a;
+        return a;
+    };
+    // put -m (rounded to fp16, as m_run holds it) into block j's spare slot,
+    // or clear it (m = 0)
+    auto set_slot = [&](int j, float m) __attribute__((always_inline)) {
+        if constexpr (kFold) {
+            const u32x4 v = {(uint32_t)from_float<ET>(-m), 0u, 0u, 0u};
+            if (half) qreg[j][DK - 1] = v;
+        }
+    };
+    bool fold_on = false;   // the fixed-maximum run: kFirst writes the slot
+
     // Per-lane LDS byte offsets inside a buffer.
     // K rows: lane reads key row l32 at d = 8*half (+16 s, +32 sub rows).
     const int k_off = (l32 * D + 8 * half) * 2;
@@ -261,7 +296,8 @@ __global__ __launch_bounds__(Geom<D>::kThreads, Geom<D>::kWavesPerSimd) void att
             for (int r = 0; r < 16; ++r) st[j][r] = 0.0f;
 #pragma unroll
         for (int s = 0; s < DK; ++s) {
-            const u32x4 a = *(const u32x4*)(buf + k_off + (32 * sub * D + 16 * s) * 2);
+            u32x4 a = *(const u32x4*)(buf + k_off + (32 * sub * D + 16 * s) * 2);
+            if (s == DK - 1) a = k_last(a);
 #pragma unroll
             for (int j = 0; j < QB; ++j) st[j] = mfma32x32x16<ET>(a, qreg[j][s], st[j]);
         }
@@ -283,9 +319,15 @@ __global__ __launch_bounds__(Geom<D>::kThreads, Geom<D>::kWavesPerSimd) void att
                 mloc = half_max(mloc);
                 s_max[j] = fmaxf(s_max[j], mloc);
                 if constexpr (MODE == kFirst) {
-                    m_run[j] = mloc * c;
+                    if constexpr (kFold) {
+                        // st is already c s (the slot is clear); m rounded to fp16
+                        m_run[j] = to_float<ET>(from_float<ET>(mloc));
+                        if (fold_on) set_slot(j, m_run[j]);
+                    } else {
+                        m_run[j] = mloc * c;
+                    }
                 } else if constexpr (MODE == kOnline) {
-                    const float mb = mloc * c;
+                    const float mb = kFold ? mloc : mloc * c;
                     if (__any(mb > m_run[j] + kRescaleSlack)) {
                         const float m_new = fmaxf(m_run[j], mb);
                         const float alpha = fast_exp2(m_run[j] - m_new);
@@ -301,8 +343,15 @@ __global__ __launch_bounds__(Geom<D>::kThreads, Geom<D>::kWavesPerSimd) void att
             // ---- p = 2^(c s - m), rounded to the input type
             const float negm = -m_run[j];
             float p[16];
+            if constexpr (kFold) {
+                // kFixed: the MFMA already subtracted m; kFirst, kOnline: the slot is clear
 #pragma unroll
-            for (int r = 0; r < 16; ++r) p[r] = fast_exp2(fmaf(st[j][r], c, negm));
+                for (int r = 0; r < 16; ++r)
+                    p[r] = fast_exp2(MODE == kFixed ? st[j][r] : st[j][r] + negm);
+            } else {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) p[r] = fast_exp2(fmaf(st[j][r], c, negm));
+            }
             if constexpr (TAIL) {
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
@@ -364,7 +413,8 @@ __global__ __launch_bounds__(Geom<D>::kThreads, Geom<D>::kWavesPerSimd) void att
                 for (int r = 0; r < 16; ++r) st[sub][j][r] = 0.0f;
 #pragma unroll
             for (int s = 0; s < DK; ++s) {
-                const u32x4 a = *(const u32x4*)(buf + k_off + (32 * sub * D + 16 * s) * 2);
+                u32x4 a = *(const u32x4*)(buf + k_off + (32 * sub * D + 16 * s) * 2);
+                if (s == DK - 1) a = k_last(a);
 #pragma unroll
                 for (int j = 0; j < QB; ++j) st[sub][j] = mfma32x32x16<ET>(a, qreg[j][s], st[sub][j]);
             }
@@ -383,8 +433,13 @@ __global__ __launch_bounds__(Geom<D>::kThreads, Geom<D>::kWavesPerSimd) void att
         auto softmax = [&](int pr) __attribute__((always_inline)) {
             const int sub = pr / QB, j = pr % QB;
             float p[16];
+            if constexpr (kFold) {
 #pragma unroll
-            for (int r = 0; r < 16; ++r) p[r] = fast_exp2(fmaf(st[sub][j][r], c, -m_run[j]));
+                for (int r = 0; r < 16; ++r) p[r] = fast_exp2(st[sub][j][r]);   // c s - m from the MFMA
+            } else {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) p[r] = fast_exp2(fmaf(st[sub][j][r], c, -m_run[j]));
+            }
 #pragma unroll
             for (int u = 0; u < 2; ++u)
 #pragma unroll
@@ -477,6 +532,7 @@ __global__ __launch_bounds__(Geom<D>::kThreads, Geom<D>::kWavesPerSimd) void att
         }
     };
 
+    fold_on = true;
     run_tiles(fixed_c);
     // Overflow vote: with m fixed at the first sub-tile's maximum, a later
     // logit larger by more than ~16 (log2) overflows the rounded p to inf,
@@ -507,6 +563,9 @@ __global__ __launch_bounds__(Geom<D>::kThreads, Geom<D>::kWavesPerSimd) void att
         __syncthreads();
         if (any) {
             reset();
+            fold_on = false;   // the online path subtracts m itself
+#pragma unroll
+            for (int j = 0; j < QB; ++j) set_slot(j, 0.0f);
             run_tiles(online_c);
         }
     }

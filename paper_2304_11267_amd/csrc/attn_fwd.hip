@@ -50,7 +50,7 @@ namespace sdattn {
 
 namespace {
 
-constexpr int kBQ = 128;               // query rows per workgroup
+constexpr int kBQ = 128;               // query rows per workgroup (64 with SMALL)
 constexpr int kKB = 64;                // keys per LDS tile
 constexpr float kRescaleSlack = 8.0f;
 constexpr int kMaxLds = 160 * 1024;
@@ -63,10 +63,15 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4_t;
 // read from LDS feeds two MFMAs (half the LDS traffic per flop) and each wave
 // carries two independent MFMA / softmax chains; the register budget is then
 // sized for two waves per SIMD.
-template <int D>
+//
+// SMALL halves the query waves of a workgroup (64 query rows instead of 128),
+// for calls whose 128-row blocks would leave CUs idle (fewer than 256
+// workgroups: the 32x32 and 16x16 levels).
+template <int D, bool SMALL = false>
 struct Geom {
     static constexpr int QB = D <= 64 ? 2 : 1;
-    static constexpr int kQW = 4 / QB;                        // query waves
+    static constexpr int kQW = (SMALL ? 2 : 4) / QB;          // query waves
+    static constexpr int kBQ = 32 * QB * kQW;                 // query rows per workgroup
     static constexpr int kWaves = 2 * kQW;                    // times two key halves
     static constexpr int kThreads = kWaves * 64;
     static constexpr int DK = (D + 15) / 16;                  // 16-deep k steps of Q K^T
@@ -98,12 +103,12 @@ __device__ __forceinline__ u32x2 lds_read_tr(const char* p) {
     return __builtin_bit_cast(u32x2, v);
 }
 
-template <int ET, int D, bool STATS, bool OROWS>
-__global__ __launch_bounds__(Geom<D>::kThreads, Geom<D>::kWavesPerSimd) void attn_fwd_lds_kernel(
+template <int ET, int D, bool STATS, bool OROWS, bool SMALL>
+__global__ __launch_bounds__((Geom<D, SMALL>::kThreads), (Geom<D, SMALL>::kWavesPerSimd)) void attn_fwd_lds_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     uint16_t* __restrict__ O, float* __restrict__ LS, int Lq, int Lk, float scale_abs, float c,
     int neg, int nqb, int oh) {
-    using G = Geom<D>;
+    using G = Geom<D, SMALL>;
     constexpr int DK = G::DK;
     constexpr int DN = G::DN;
     constexpr int QB = G::QB;
@@ -125,7 +130,7 @@ __global__ __launch_bounds__(Geom<D>::kThreads, Geom<D>::kWavesPerSimd) void att
     const int tile = xcd_remap(blockIdx.x, gridDim.x);
     const int bh = tile / nqb;
     const int qb = tile - bh * nqb;
-    const int q0 = qb * kBQ + wq * 32 * QB;   // first row of this wave's QB blocks
+    const int q0 = qb * G::kBQ + wq * 32 * QB;   // first row of this wave's QB blocks
 
     const char* Kh = (const char*)(K + (size_t)bh * Lk * D);
     const char* Vh = (const char*)(V + (size_t)bh * Lk * D);
@@ -645,37 +650,39 @@ __global__ __launch_bounds__(Geom<D>::kThreads, Geom<D>::kWavesPerSimd) void att
     }
 }
 
+template <int ET, int D, bool STATS, bool OROWS, bool SMALL>
+hipError_t launch_kernel(const AttnArgs& a) {
+    using G = Geom<D, SMALL>;
+    const int nqb = (a.Lq + G::kBQ - 1) / G::kBQ;
+    const long long nblk = (long long)a.B * a.H * nqb;
+    const float scale_abs = a.scale < 0 ? -a.scale : a.scale;
+    const float c = scale_abs * kLog2e;
+    auto kern = attn_fwd_lds_kernel<ET, D, STATS, OROWS, SMALL>;
+    static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                                       hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                       G::kLdsBytes);
+    if (attr != hipSuccess) return attr;
+    hipLaunchKernelGGL(kern, dim3((unsigned)nblk), dim3(G::kThreads), G::kLdsBytes,
+                       (hipStream_t)a.stream, (const uint16_t*)a.q, (const uint16_t*)a.k,
+                       (const uint16_t*)a.v, (uint16_t*)a.out, a.ls, a.Lq, a.Lk, scale_abs, c,
+                       a.scale < 0 ? 1 : 0, nqb, a.o_rows ? a.H : 0);
+    return hipGetLastError();
+}
+
 template <int ET, int D>
 hipError_t launch_d(const AttnArgs& a) {
-    using G = Geom<D>;
-    if constexpr (!G::kFits) {
+    if constexpr (!Geom<D>::kFits || !Geom<D, true>::kFits) {
         return launch_attn_fwd_generic(a);
     } else {
-        const int nqb = (a.Lq + kBQ - 1) / kBQ;
-        const long long nblk = (long long)a.B * a.H * nqb;
-        const float scale_abs = a.scale < 0 ? -a.scale : a.scale;
-        const float c = scale_abs * kLog2e;
-        static const hipError_t attr0 = hipFuncSetAttribute(
-            reinterpret_cast<const void*>(&attn_fwd_lds_kernel<ET, D, false, false>),
-            hipFuncAttributeMaxDynamicSharedMemorySize, G::kLdsBytes);
-        static const hipError_t attr1 = hipFuncSetAttribute(
-            reinterpret_cast<const void*>(&attn_fwd_lds_kernel<ET, D, true, false>),
-            hipFuncAttributeMaxDynamicSharedMemorySize, G::kLdsBytes);
-        static const hipError_t attr2 = hipFuncSetAttribute(
-            reinterpret_cast<const void*>(&attn_fwd_lds_kernel<ET, D, false, true>),
-            hipFuncAttributeMaxDynamicSharedMemorySize, G::kLdsBytes);
-        if (attr0 != hipSuccess) return attr0;
-        if (attr1 != hipSuccess) return attr1;
-        if (attr2 != hipSuccess) return attr2;
         if (a.ls && a.o_rows) return hipErrorInvalidValue;   // no caller asks for both
-        auto kern = a.ls       ? attn_fwd_lds_kernel<ET, D, true, false>
-                    : a.o_rows ? attn_fwd_lds_kernel<ET, D, false, true>
-                               : attn_fwd_lds_kernel<ET, D, false, false>;
-        hipLaunchKernelGGL(kern, dim3((unsigned)nblk), dim3(G::kThreads),
-                           G::kLdsBytes, (hipStream_t)a.stream, (const uint16_t*)a.q,
-                           (const uint16_t*)a.k, (const uint16_t*)a.v, (uint16_t*)a.out, a.ls,
-                           a.Lq, a.Lk, scale_abs, c, a.scale < 0 ? 1 : 0, nqb, a.o_rows ? a.H : 0);
-        return hipGetLastError();
+        if (a.ls) return launch_kernel<ET, D, true, false, false>(a);
+        // the smaller workgroups when the 128-row ones would not cover the CUs
+        const bool small = (long long)a.B * a.H * ((a.Lq + kBQ - 1) / kBQ) < 256;
+        if (a.o_rows)
+            return small ? launch_kernel<ET, D, false, true, true>(a)
+                         : launch_kernel<ET, D, false, true, false>(a);
+        return small ? launch_kernel<ET, D, false, false, true>(a)
+                     : launch_kernel<ET, D, false, false, false>(a);
     }
 }
 
@@ -689,7 +696,8 @@ hipError_t dispatch_d(const AttnArgs& a, std::integer_sequence<int, Ds...>) {
 }  // namespace
 
 long long attn_fwd_grid(int B, int H, int Lq) {
-    return (long long)B * H * ((Lq + kBQ - 1) / kBQ);
+    // the largest grid any geometry launches (32-row blocks bound it)
+    return (long long)B * H * ((Lq + 31) / 32);
 }
 
 hipError_t launch_attn_fwd(const AttnArgs& a) {

@@ -528,13 +528,23 @@ __global__ __launch_bounds__((Geom<D, SMALL>::kThreads), (Geom<D, SMALL>::kWaves
         }
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
+        // Inside the loop only whole tiles are consumed; a ragged last tile
+        // (the last tile of its half: nothing is copied over it afterwards)
+        // waits in its buffer until the loop ends.  With a single way through
+        // the loop body the accumulators keep their registers across
+        // iterations instead of being copied at a join.
+        int pend = -1;
         for (int i = 1; i < nh; ++i) {
             const int b = i & 1;
             if (i + 1 < t_count) issue_tile(t_first + i + 1, b ^ 1);
-            if (i < t_count) consume(mode_c, mode_c, t_first + i, b);
+            if (i < t_count) {
+                if ((t_first + i + 1) * kKB <= Lk) consume(mode_c, mode_c, t_first + i, b);
+                else pend = i;
+            }
             __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
         }
+        if (pend >= 0) consume(mode_c, mode_c, t_first + pend, pend & 1);
     };
 
     fold_on = true;

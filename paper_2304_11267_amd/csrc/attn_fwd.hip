@@ -162,15 +162,17 @@ __global__ __launch_bounds__((Geom<D, SMALL>::kThreads), (Geom<D, SMALL>::kWaves
         const int kbase = t * kKB;
         char* bufp = hbase + b * G::kBufBytes;
         if (kbase + kKB <= Lk) {
-            // a full tile is one contiguous run of K (and of V) rows
-            const size_t tile_off = (size_t)kbase * (2 * D) + lane * 16;
+            // a full tile is one contiguous run of K (and of V) rows; byte
+            // offsets inside a head fit 32 bits (the launch checks Lk * D)
+            const uint32_t tile_off = (uint32_t)kbase * (2 * D) + lane * 16;
 #pragma unroll
             for (int i = 0; i < (2 * G::kChunks + kQW - 1) / kQW; ++i) {
                 const int cidx = wq + kQW * i;
                 if (cidx < 2 * G::kChunks) {
                     const bool isv = cidx >= G::kChunks;
                     const int cc = isv ? cidx - G::kChunks : cidx;
-                    __builtin_amdgcn_global_load_lds((isv ? Vh : Kh) + tile_off + cc * 1024,
+                    const char* src = isv ? Vh : Kh;
+                    __builtin_amdgcn_global_load_lds(src + (size_t)(tile_off + cc * 1024),
                                                      (lds_void_t*)(bufp + (isv ? TB : 0) + cc * 1024),
                                                      16, 0, 0);
                 }
@@ -685,6 +687,8 @@ hipError_t launch_d(const AttnArgs& a) {
         return launch_attn_fwd_generic(a);
     } else {
         if (a.ls && a.o_rows) return hipErrorInvalidValue;   // no caller asks for both
+        // tile copies address a head's K and V with 32-bit byte offsets
+        if ((long long)a.Lk * D * 2 > 0x7fffffffLL) return launch_attn_fwd_generic(a);
         if (a.ls) return launch_kernel<ET, D, true, false, false>(a);
         // the smaller workgroups when the 128-row ones would not cover the CUs
         const bool small = (long long)a.B * a.H * ((a.Lq + kBQ - 1) / kBQ) < 256;

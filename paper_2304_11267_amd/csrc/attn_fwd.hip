@@ -85,8 +85,12 @@ struct Geom {
     static constexpr int kMergeBytes = kQW * kMergeFloats * 4;
     static constexpr int kLdsBytes = 2 * kHalfBytes > kMergeBytes ? 2 * kHalfBytes : kMergeBytes;
     static constexpr bool kFits = D >= 32 && D % 8 == 0 && kLdsBytes <= kMaxLds;
-    // waves per SIMD the register budget is sized for (2: 256 VGPRs each)
-    static constexpr int kWavesPerSimd = 2;
+    // Waves per SIMD the register budget is sized for: two (256 registers
+    // each) when the LDS lets enough workgroups share a CU, else one, which
+    // leaves a wave up to 512 registers (the matrix-core registers then take
+    // what would otherwise spill to scratch) at no cost in occupancy.
+    static constexpr int kWgPerCu = kLdsBytes <= kMaxLds ? kMaxLds / kLdsBytes : 1;
+    static constexpr int kWavesPerSimd = kWgPerCu * kWaves >= 8 ? 2 : 1;
 };
 
 // Logical tile for workgroup `bid`.  Workgroups are dealt round-robin over the

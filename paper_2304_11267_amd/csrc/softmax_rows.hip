@@ -12,6 +12,13 @@
 // Two pairs merge as (m, s) + (m', s') = (M, s e^{m-M} + s' e^{m'-M}),
 // M = max(m, m'), which is exact in real arithmetic and order-free.
 // The optional second pass re-reads the row (now in L2) and writes p.
+//
+// Rows of at most 64 * 16 chunks whose p is wanted (and short rows) take a
+// register-resident variant: a wave
+// holds its whole row (R chunks per lane, all loads issued at once), takes
+// the exact maximum (stage 1 in the lane, stage 2 across the wave), then the
+// sum of the exponentials the same way, and writes p from the exponentials it
+// already holds -- the row is read from memory once.
 #include "device.h"
 #include "launch.h"
 
@@ -166,6 +173,78 @@ __global__ __launch_bounds__(kThreads) void softmax_rows_kernel(
     }
 }
 
+// One row per wave, held in registers: R chunks per lane (64 * R >= chunks).
+template <int ET, int R>
+__global__ __launch_bounds__(kThreads) void softmax_rows_reg_kernel(
+    const void* __restrict__ A, float* __restrict__ LS, void* __restrict__ P, long long rows,
+    long long cols, float scale, long long ngroups) {
+    constexpr int EPC = Elem<ET>::kPerChunk;
+    const int lane = lane_id();
+    const int wave = threadIdx.x >> 6;
+    const int nunits = (int)(cols / EPC);
+
+    for (long long g = blockIdx.x; g < ngroups; g += gridDim.x) {
+        const long long row = g * 4 + wave;
+        if (row >= rows) continue;   // no barriers below: waves are independent
+        const long long base = row * nunits;
+        float x[R][EPC];
+#pragma unroll
+        for (int i = 0; i < R; ++i) {
+            if (lane + 64 * i < nunits) load_chunk<ET>(A, base + lane + 64 * i, x[i]);
+        }
+        // exact row maximum of scale * a
+        float m = -__builtin_inff();
+#pragma unroll
+        for (int i = 0; i < R; ++i)
+            if (lane + 64 * i < nunits) {
+#pragma unroll
+                for (int e = 0; e < EPC; ++e) {
+                    x[i][e] *= scale;
+                    m = fmaxf(m, x[i][e]);
+                }
+            }
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+        // exponentials (kept for p) and their sum
+        const float nb = -m * kLog2e;
+        float s = 0.0f;
+#pragma unroll
+        for (int i = 0; i < R; ++i)
+            if (lane + 64 * i < nunits) {
+#pragma unroll
+                for (int e = 0; e < EPC; ++e) {
+                    x[i][e] = fast_exp2(fmaf(x[i][e], kLog2e, nb));
+                    s += x[i][e];
+                }
+            }
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
+        if (lane == 0) {
+            LS[2 * row] = m;
+            LS[2 * row + 1] = s;
+        }
+        if (P) {
+            const float inv = 1.0f / s;
+#pragma unroll
+            for (int i = 0; i < R; ++i)
+                if (lane + 64 * i < nunits) {
+#pragma unroll
+                    for (int e = 0; e < EPC; ++e) x[i][e] *= inv;
+                    store_chunk<ET>(P, base + lane + 64 * i, x[i]);
+                }
+        }
+    }
+}
+
+template <int ET, int R>
+hipError_t launch_reg(const SoftmaxArgs& a) {
+    const long long ngroups = (a.rows + 3) / 4;
+    const long long grid = ngroups < kMaxGrid ? ngroups : kMaxGrid;
+    hipLaunchKernelGGL((softmax_rows_reg_kernel<ET, R>), dim3((unsigned)grid), dim3(kThreads), 0,
+                       (hipStream_t)a.stream, a.a, a.ls, a.p, a.rows, a.cols, a.scale, ngroups);
+    return hipGetLastError();
+}
+
 template <int ET, int WPR, bool VEC>
 hipError_t launch3(const SoftmaxArgs& a) {
     constexpr int RPW = 4 / WPR;
@@ -179,6 +258,17 @@ hipError_t launch3(const SoftmaxArgs& a) {
 template <int ET>
 hipError_t launch_et(const SoftmaxArgs& a) {
     const bool vec = a.cols % Elem<ET>::kPerChunk == 0;
+    const long long chunks = a.cols / Elem<ET>::kPerChunk;
+    // Register rows pay off when p is written (no second read) and for short
+    // rows; the statistics alone of longer rows stream faster (measured: more
+    // waves in flight with the few registers the streaming kernel needs).
+    if (vec && (a.p != nullptr || chunks <= 128)) {
+        if (chunks <= 64) return launch_reg<ET, 1>(a);
+        if (chunks <= 128) return launch_reg<ET, 2>(a);
+        if (chunks <= 256) return launch_reg<ET, 4>(a);
+        if (chunks <= 512) return launch_reg<ET, 8>(a);
+        if (chunks <= 1024) return launch_reg<ET, 16>(a);
+    }
     const bool wide = a.cols > 16384;
     if (wide) return vec ? launch3<ET, 4, true>(a) : launch3<ET, 4, false>(a);
     return vec ? launch3<ET, 1, true>(a) : launch3<ET, 1, false>(a);

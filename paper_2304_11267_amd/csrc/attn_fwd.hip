@@ -5,8 +5,11 @@
 // split in two halves over the key tiles (the first half of the tiles and the
 // second), and at the end the two halves of every row are merged through LDS.
 // A wave owns QB blocks of 32 query rows: QB = 2 when D <= 64 (4 waves per
-// workgroup, two per SIMD, up to 256 VGPRs each), QB = 1 above (8 waves).
-// With QB = 2 every K and V^T operand read from LDS feeds two MFMAs.
+// workgroup), QB = 1 above (8 waves).  With QB = 2 every K and V^T operand
+// read from LDS feeds two MFMAs.  Registers are budgeted for two waves per
+// SIMD (256 each), or for one (up to 512) where the LDS already limits a CU
+// to one wave per SIMD.  Grids that would leave CUs idle use workgroups of 64
+// query rows (half the query waves).
 // Key/value tiles of 64 keys move through LDS double-buffered per half: while
 // one tile is consumed the next is copied straight from global memory
 // (global_load_lds, 16 bytes per lane, no registers involved), keeping the
@@ -17,7 +20,10 @@
 //                    The accumulator puts one query per lane (lane % 32) and
 //                    16 of the 32 keys in that lane, so the row maximum needs a
 //                    single exchange between lane halves.
-//   p = 2^(c s - m)  c = |scale| log2(e).  m is fixed at the maximum of each
+//   p = 2^(c s - m)  c = |scale| log2(e).  For fp16 with D % 16 == 8 the
+//                    MFMA itself returns c s - m (Q pre-scaled by c, -m in the
+//                    spare contraction slot against a 1 in K's padding).
+//                    m is fixed at the maximum of each
 //                    wave's first sub-tile (p may then exceed 1); a row whose
 //                    later logits would overflow the rounded p sends the
 //                    workgroup through an exact fallback in which m moves, with

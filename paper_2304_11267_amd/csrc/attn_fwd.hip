@@ -1,16 +1,17 @@
 // attn_fwd.hip -- single-pass attention forward (Eq. 3) for gfx950, with the
 // K and V tiles streamed into LDS by direct global->LDS copies.
 //
-// One workgroup covers 128 query rows of one (batch, head).  Its waves are
+// One workgroup covers 128 query rows of one (batch, head) (64 or 256 in the
+// other geometries, see Geom).  Its waves are
 // split in two halves over the key tiles (the first half of the tiles and the
 // second), and at the end the two halves of every row are merged through LDS.
 // A wave owns QB blocks of 32 query rows: QB = 2 when D <= 64 (4 waves per
 // workgroup), QB = 1 above (8 waves).  With QB = 2 every K and V^T operand
 // read from LDS feeds two MFMAs.  Registers are budgeted for two waves per
 // SIMD (256 each), or for one (up to 512) where the LDS already limits a CU
-// to one wave per SIMD.  Grids that would leave CUs idle use workgroups of 64
-// query rows (half the query waves).
-// Key/value tiles of 64 keys move through LDS double-buffered per half: while
+// to one wave per SIMD.
+// Key/value tiles of 64 keys (128 with 256-row workgroups) move through LDS
+// double-buffered per half: while
 // one tile is consumed the next is copied straight from global memory
 // (global_load_lds, 16 bytes per lane, no registers involved), keeping the
 // row-major [key][d] layout.  Per 32-key sub-tile, wave and query block:
@@ -20,10 +21,8 @@
 //                    The accumulator puts one query per lane (lane % 32) and
 //                    16 of the 32 keys in that lane, so the row maximum needs a
 //                    single exchange between lane halves.
-//   p = 2^(c s - m)  c = |scale| log2(e).  For fp16 with D % 16 == 8 the
-//                    MFMA itself returns c s - m (Q pre-scaled by c, -m in the
-//                    spare contraction slot against a 1 in K's padding).
-//                    m is fixed at the maximum of each
+//   p = 2^(c s - m)  c = |scale| log2(e), one FMA and one exponential per
+//                    score.  m is fixed at the maximum of each
 //                    wave's first sub-tile (p may then exceed 1); a row whose
 //                    later logits would overflow the rounded p sends the
 //                    workgroup through an exact fallback in which m moves, with
@@ -56,8 +55,11 @@ namespace sdattn {
 
 namespace {
 
-constexpr int kBQ = 128;               // query rows per workgroup (64 with SMALL)
-constexpr int kKB = 64;                // keys per LDS tile
+// Workgroup geometries (the GEO template argument): rows of queries per
+// workgroup and keys per LDS tile.
+constexpr int kGeoSmall = 0;           // 64 rows, 64-key tiles
+constexpr int kGeoNormal = 1;          // 128 rows, 64-key tiles
+constexpr int kGeoBig = 2;             // 256 rows, 128-key tiles (QB = 2 only)
 constexpr float kRescaleSlack = 8.0f;
 constexpr int kMaxLds = 160 * 1024;
 
@@ -70,27 +72,32 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4_t;
 // carries two independent MFMA / softmax chains; the register budget is then
 // sized for two waves per SIMD.
 //
-// SMALL halves the query waves of a workgroup (64 query rows instead of 128),
-// for calls whose 128-row blocks would leave CUs idle (fewer than 256
-// workgroups: the 32x32 and 16x16 levels).
-template <int D, bool SMALL = false>
+// kGeoSmall halves the query waves of a workgroup (64 query rows instead of
+// 128), for calls whose 128-row blocks would leave CUs idle (fewer than 256
+// workgroups: the 32x32 and 16x16 levels).  kGeoBig doubles them (256 rows,
+// eight waves) and the keys per tile (128), for grids that still cover the
+// CUs: each K/V tile then serves twice the queries and a barrier twice the
+// keys, in the LDS the two 128-row workgroups of a CU would otherwise hold.
+template <int D, int GEO = kGeoNormal>
 struct Geom {
     static constexpr int QB = D <= 64 ? 2 : 1;
-    static constexpr int kQW = (SMALL ? 2 : 4) / QB;          // query waves
+    static constexpr bool kBig = GEO == kGeoBig;
+    static constexpr int kTK = kBig ? 128 : 64;               // keys per LDS tile
+    static constexpr int kQW = kBig ? 4 : (GEO == kGeoSmall ? 2 : 4) / QB;   // query waves
     static constexpr int kBQ = 32 * QB * kQW;                 // query rows per workgroup
     static constexpr int kWaves = 2 * kQW;                    // times two key halves
     static constexpr int kThreads = kWaves * 64;
     static constexpr int DK = (D + 15) / 16;                  // 16-deep k steps of Q K^T
     static constexpr int DN = (D + 31) / 32;                  // 32-row d tiles of O^T
     static constexpr bool kOnes = (D % 32) != 0;              // padding rows carry the row sum
-    static constexpr int kTileBytes = kKB * D * 2;            // one K or V tile
+    static constexpr int kTileBytes = kTK * D * 2;            // one K or V tile
     static constexpr int kChunks = kTileBytes / 1024;         // 1 KiB wave copies per tile
     static constexpr int kBufBytes = kTileBytes * (kOnes ? 3 : 2);   // K, V (, constant block)
     static constexpr int kHalfBytes = 2 * kBufBytes;          // two buffers per key half
     static constexpr int kMergeFloats = QB * (DN * 16 * 64 + 3 * 64);   // one wave's O^T, m, max, l
     static constexpr int kMergeBytes = kQW * kMergeFloats * 4;
     static constexpr int kLdsBytes = 2 * kHalfBytes > kMergeBytes ? 2 * kHalfBytes : kMergeBytes;
-    static constexpr bool kFits = D >= 32 && D % 8 == 0 && kLdsBytes <= kMaxLds;
+    static constexpr bool kFits = D >= 32 && D % 8 == 0 && kLdsBytes <= kMaxLds && (!kBig || QB == 2);
     // Waves per SIMD the register budget is sized for: two (256 registers
     // each) when the LDS lets enough workgroups share a CU, else one, which
     // leaves a wave up to 512 registers (the matrix-core registers then take
@@ -113,12 +120,12 @@ __device__ __forceinline__ u32x2 lds_read_tr(const char* p) {
     return __builtin_bit_cast(u32x2, v);
 }
 
-template <int ET, int D, bool STATS, bool OROWS, bool SMALL>
-__global__ __launch_bounds__((Geom<D, SMALL>::kThreads), (Geom<D, SMALL>::kWavesPerSimd)) void attn_fwd_lds_kernel(
+template <int ET, int D, bool STATS, bool OROWS, int GEO>
+__global__ __launch_bounds__((Geom<D, GEO>::kThreads), (Geom<D, GEO>::kWavesPerSimd)) void attn_fwd_lds_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,
     uint16_t* __restrict__ O, float* __restrict__ LS, int Lq, int Lk, float scale_abs, float c,
     int neg, int nqb, int oh) {
-    using G = Geom<D, SMALL>;
+    using G = Geom<D, GEO>;
     constexpr int DK = G::DK;
     constexpr int DN = G::DN;
     constexpr int QB = G::QB;
@@ -160,7 +167,8 @@ __global__ __launch_bounds__((Geom<D, SMALL>::kThreads), (Geom<D, SMALL>::kWaves
 
     // Tiles of this half: [t_first, t_first + t_count).  Half 0 takes the
     // first ceil(ntiles / 2), half 1 the rest; both run nh steps.
-    const int ntiles = (Lk + kKB - 1) / kKB;
+    constexpr int kTK = G::kTK;
+    const int ntiles = (Lk + kTK - 1) / kTK;
     const int nh = (ntiles + 1) / 2;
     const int t_first = kh ? nh : 0;
     const int t_count = kh ? ntiles - nh : nh;
@@ -169,9 +177,9 @@ __global__ __launch_bounds__((Geom<D, SMALL>::kThreads), (Geom<D, SMALL>::kWaves
     // the 1 KiB pieces wq, wq + kQW, ...).  Rows past Lk repeat row Lk - 1
     // (finite data; their weights are forced to zero).
     auto issue_tile = [&](int t, int b) __attribute__((always_inline)) {
-        const int kbase = t * kKB;
+        const int kbase = t * kTK;
         char* bufp = hbase + b * G::kBufBytes;
-        if (kbase + kKB <= Lk) {
+        if (kbase + kTK <= Lk) {
             // a full tile is one contiguous run of K (and of V) rows; byte
             // offsets inside a head fit 32 bits (the launch checks Lk * D)
             const uint32_t tile_off = (uint32_t)kbase * (2 * D) + lane * 16;
@@ -220,40 +228,6 @@ __global__ __launch_bounds__((Geom<D, SMALL>::kThreads), (Geom<D, SMALL>::kWaves
             qreg[j][s] = v;
         }
 
-    // The shift folded into Q K^T (fp16, no statistics, D % 16 == 8): Q is
-    // scaled by c once, and the spare k slot d = D of the last k-step holds
-    // -m in Q against a constant 1 in K, so the MFMA returns c s - m and the
-    // exponent needs no per-score FMA.  m is rounded to fp16 first; any
-    // reference value works, as long as every key of the row uses the same.
-    constexpr bool kFold = ET == kF16 && !STATS && D % 16 == 8;
-    if constexpr (kFold) {
-#pragma unroll
-        for (int j = 0; j < QB; ++j)
-#pragma unroll
-            for (int s = 0; s < DK; ++s)
-#pragma unroll
-                for (int w = 0; w < 4; ++w) {
-                    const uint32_t x = qreg[j][s][w];
-                    qreg[j][s][w] = pack2<ET>(to_float<ET>((uint16_t)(x & 0xffffu)) * c,
-                                              to_float<ET>((uint16_t)(x >> 16)) * c);
-                }
-    }
-    // K operand of the last k-step for the lanes holding d = D .. D + 7: a 1
-    // at d = D, zeros after (used only when kFold)
-    const u32x4 kone = {(uint32_t)from_float<ET>(1.0f), 0u, 0u, 0u};
-    auto k_last = [&](u32x4 a) __attribute__((always_inline)) -> u32x4 {
-        if constexpr (kFold) return half ? kone : a;
-        return a;
-    };
-    // put -m (rounded to fp16, as m_run holds it) into block j's spare slot,
-    // or clear it (m = 0)
-    auto set_slot = [&](int j, float m) __attribute__((always_inline)) {
-        if constexpr (kFold) {
-            const u32x4 v = {(uint32_t)from_float<ET>(-m), 0u, 0u, 0u};
-            if (half) qreg[j][DK - 1] = v;
-        }
-    };
-    bool fold_on = false;   // the fixed-maximum run: kFirst writes the slot
 
     // Per-lane LDS byte offsets inside a buffer.
     // K rows: lane reads key row l32 at d = 8*half (+16 s, +32 sub rows).
@@ -314,7 +288,6 @@ __global__ __launch_bounds__((Geom<D, SMALL>::kThreads), (Geom<D, SMALL>::kWaves
 #pragma unroll
         for (int s = 0; s < DK; ++s) {
             u32x4 a = *(const u32x4*)(buf + k_off + (32 * sub * D + 16 * s) * 2);
-            if (s == DK - 1) a = k_last(a);
 #pragma unroll
             for (int j = 0; j < QB; ++j) st[j] = mfma32x32x16<ET>(a, qreg[j][s], st[j]);
         }
@@ -336,15 +309,9 @@ __global__ __launch_bounds__((Geom<D, SMALL>::kThreads), (Geom<D, SMALL>::kWaves
                 mloc = half_max(mloc);
                 s_max[j] = fmaxf(s_max[j], mloc);
                 if constexpr (MODE == kFirst) {
-                    if constexpr (kFold) {
-                        // st is already c s (the slot is clear); m rounded to fp16
-                        m_run[j] = to_float<ET>(from_float<ET>(mloc));
-                        if (fold_on) set_slot(j, m_run[j]);
-                    } else {
-                        m_run[j] = mloc * c;
-                    }
+                    m_run[j] = mloc * c;
                 } else if constexpr (MODE == kOnline) {
-                    const float mb = kFold ? mloc : mloc * c;
+                    const float mb = mloc * c;
                     if (__any(mb > m_run[j] + kRescaleSlack)) {
                         const float m_new = fmaxf(m_run[j], mb);
                         const float alpha = fast_exp2(m_run[j] - m_new);
@@ -360,15 +327,8 @@ __global__ __launch_bounds__((Geom<D, SMALL>::kThreads), (Geom<D, SMALL>::kWaves
             // ---- p = 2^(c s - m), rounded to the input type
             const float negm = -m_run[j];
             float p[16];
-            if constexpr (kFold) {
-                // kFixed: the MFMA already subtracted m; kFirst, kOnline: the slot is clear
 #pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    p[r] = fast_exp2(MODE == kFixed ? st[j][r] : st[j][r] + negm);
-            } else {
-#pragma unroll
-                for (int r = 0; r < 16; ++r) p[r] = fast_exp2(fmaf(st[j][r], c, negm));
-            }
+            for (int r = 0; r < 16; ++r) p[r] = fast_exp2(fmaf(st[j][r], c, negm));
             if constexpr (TAIL) {
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
@@ -431,8 +391,7 @@ __global__ __launch_bounds__((Geom<D, SMALL>::kThreads), (Geom<D, SMALL>::kWaves
 #pragma unroll
             for (int s = 0; s < DK; ++s) {
                 u32x4 a = *(const u32x4*)(buf + k_off + (32 * sub * D + 16 * s) * 2);
-                if (s == DK - 1) a = k_last(a);
-#pragma unroll
+    #pragma unroll
                 for (int j = 0; j < QB; ++j) st[sub][j] = mfma32x32x16<ET>(a, qreg[j][s], st[sub][j]);
             }
         };
@@ -450,13 +409,8 @@ __global__ __launch_bounds__((Geom<D, SMALL>::kThreads), (Geom<D, SMALL>::kWaves
         auto softmax = [&](int pr) __attribute__((always_inline)) {
             const int sub = pr / QB, j = pr % QB;
             float p[16];
-            if constexpr (kFold) {
 #pragma unroll
-                for (int r = 0; r < 16; ++r) p[r] = fast_exp2(st[sub][j][r]);   // c s - m from the MFMA
-            } else {
-#pragma unroll
-                for (int r = 0; r < 16; ++r) p[r] = fast_exp2(fmaf(st[sub][j][r], c, -m_run[j]));
-            }
+            for (int r = 0; r < 16; ++r) p[r] = fast_exp2(fmaf(st[sub][j][r], c, -m_run[j]));
 #pragma unroll
             for (int u = 0; u < 2; ++u)
 #pragma unroll
@@ -508,23 +462,31 @@ __global__ __launch_bounds__((Geom<D, SMALL>::kThreads), (Geom<D, SMALL>::kWaves
     };
 
     // consume the tile t (in buffer b) of this half; its first sub-tile in
-    // mode mode0_c, the second in mode_c
+    // mode mode0_c, the others in mode_c.  A pipelined 64-key step reads its
+    // rows relative to the pointer it gets, so a 128-key tile is two of them.
     auto consume = [&](auto mode0_c, auto mode_c, int t, int b) __attribute__((always_inline)) {
         const char* buf = hbase + b * G::kBufBytes;
-        const int kbase = t * kKB;
+        const int kbase = t * kTK;
         constexpr bool kPipelined = decltype(mode0_c)::value == kFixed &&
                                     decltype(mode_c)::value == kFixed && !STATS;
-        if (kbase + kKB <= Lk) {
+        if (kbase + kTK <= Lk) {
             if constexpr (kPipelined) {
-                tile_fixed(buf);
+#pragma unroll
+                for (int h = 0; h < kTK / 64; ++h) tile_fixed(buf + h * 64 * D * 2);
             } else {
                 step32(mode0_c, full_c, buf, 0, kbase);
-                step32(mode_c, full_c, buf, 1, kbase + 32);
+#pragma unroll
+                for (int sb = 1; sb < kTK / 32; ++sb) step32(mode_c, full_c, buf, sb, kbase + 32 * sb);
             }
         } else {
             if (kbase + 32 <= Lk) step32(mode0_c, full_c, buf, 0, kbase);
             else step32(mode0_c, tail_c, buf, 0, kbase);
-            if (kbase + 32 < Lk) step32(mode_c, tail_c, buf, 1, kbase + 32);
+#pragma unroll
+            for (int sb = 1; sb < kTK / 32; ++sb) {
+                const int kb = kbase + 32 * sb;
+                if (kb + 32 <= Lk) step32(mode_c, full_c, buf, sb, kb);
+                else if (kb < Lk) step32(mode_c, tail_c, buf, sb, kb);
+            }
         }
     };
 
@@ -550,7 +512,7 @@ __global__ __launch_bounds__((Geom<D, SMALL>::kThreads), (Geom<D, SMALL>::kWaves
             const int b = i & 1;
             if (i + 1 < t_count) issue_tile(t_first + i + 1, b ^ 1);
             if (i < t_count) {
-                if ((t_first + i + 1) * kKB <= Lk) consume(mode_c, mode_c, t_first + i, b);
+                if ((t_first + i + 1) * kTK <= Lk) consume(mode_c, mode_c, t_first + i, b);
                 else pend = i;
             }
             __builtin_amdgcn_s_waitcnt(0);
@@ -559,7 +521,6 @@ __global__ __launch_bounds__((Geom<D, SMALL>::kThreads), (Geom<D, SMALL>::kWaves
         if (pend >= 0) consume(mode_c, mode_c, t_first + pend, pend & 1);
     };
 
-    fold_on = true;
     run_tiles(fixed_c);
     // Overflow vote: with m fixed at the first sub-tile's maximum, a later
     // logit larger by more than ~16 (log2) overflows the rounded p to inf,
@@ -590,9 +551,6 @@ __global__ __launch_bounds__((Geom<D, SMALL>::kThreads), (Geom<D, SMALL>::kWaves
         __syncthreads();
         if (any) {
             reset();
-            fold_on = false;   // the online path subtracts m itself
-#pragma unroll
-            for (int j = 0; j < QB; ++j) set_slot(j, 0.0f);
             run_tiles(online_c);
         }
     }
@@ -672,14 +630,14 @@ __global__ __launch_bounds__((Geom<D, SMALL>::kThreads), (Geom<D, SMALL>::kWaves
     }
 }
 
-template <int ET, int D, bool STATS, bool OROWS, bool SMALL>
+template <int ET, int D, bool STATS, bool OROWS, int GEO>
 hipError_t launch_kernel(const AttnArgs& a) {
-    using G = Geom<D, SMALL>;
+    using G = Geom<D, GEO>;
     const int nqb = (a.Lq + G::kBQ - 1) / G::kBQ;
     const long long nblk = (long long)a.B * a.H * nqb;
     const float scale_abs = a.scale < 0 ? -a.scale : a.scale;
     const float c = scale_abs * kLog2e;
-    auto kern = attn_fwd_lds_kernel<ET, D, STATS, OROWS, SMALL>;
+    auto kern = attn_fwd_lds_kernel<ET, D, STATS, OROWS, GEO>;
     static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                                        hipFuncAttributeMaxDynamicSharedMemorySize,
                                                        G::kLdsBytes);
@@ -693,20 +651,27 @@ hipError_t launch_kernel(const AttnArgs& a) {
 
 template <int ET, int D>
 hipError_t launch_d(const AttnArgs& a) {
-    if constexpr (!Geom<D>::kFits || !Geom<D, true>::kFits) {
+    if constexpr (!Geom<D, kGeoNormal>::kFits || !Geom<D, kGeoSmall>::kFits) {
         return launch_attn_fwd_generic(a);
     } else {
         if (a.ls && a.o_rows) return hipErrorInvalidValue;   // no caller asks for both
         // tile copies address a head's K and V with 32-bit byte offsets
         if ((long long)a.Lk * D * 2 > 0x7fffffffLL) return launch_attn_fwd_generic(a);
-        if (a.ls) return launch_kernel<ET, D, true, false, false>(a);
-        // the smaller workgroups when the 128-row ones would not cover the CUs
-        const bool small = (long long)a.B * a.H * ((a.Lq + kBQ - 1) / kBQ) < 256;
-        if (a.o_rows)
-            return small ? launch_kernel<ET, D, false, true, true>(a)
-                         : launch_kernel<ET, D, false, true, false>(a);
-        return small ? launch_kernel<ET, D, false, false, true>(a)
-                     : launch_kernel<ET, D, false, false, false>(a);
+        if (a.ls) return launch_kernel<ET, D, true, false, kGeoNormal>(a);
+        // the geometry with the largest workgroups whose grid still covers the
+        // 256 CUs (the smallest one when none does)
+        const long long heads = (long long)a.B * a.H;
+        const bool small = heads * ((a.Lq + 127) / 128) < 256;
+        bool big = false;
+        if constexpr (Geom<D, kGeoBig>::kFits) big = heads * ((a.Lq + 255) / 256) >= 256;
+        if (small) return a.o_rows ? launch_kernel<ET, D, false, true, kGeoSmall>(a)
+                                   : launch_kernel<ET, D, false, false, kGeoSmall>(a);
+        if constexpr (Geom<D, kGeoBig>::kFits) {
+            if (big) return a.o_rows ? launch_kernel<ET, D, false, true, kGeoBig>(a)
+                                     : launch_kernel<ET, D, false, false, kGeoBig>(a);
+        }
+        return a.o_rows ? launch_kernel<ET, D, false, true, kGeoNormal>(a)
+                        : launch_kernel<ET, D, false, false, kGeoNormal>(a);
     }
 }
 

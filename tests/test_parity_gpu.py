@@ -43,15 +43,20 @@ def run_forward(q, k, v, scale, dtype="f16", want_ls=False):
 
 
 def check_case(q, k, v, scale, dtype="f16", rows=None, what=""):
+    """Both launches against the oracle: the plain one (the configuration the
+    benchmark times) and the one that also returns Eq. 4's statistics."""
+    g_plain = run_forward(q, k, v, scale, dtype)
     g, ls = run_forward(q, k, v, scale, dtype, want_ls=True)
     r, L, S = oracle.attention(q, k, v, scale, rows=rows, dtype="bf16" if dtype == "bf16" else None)
     D = q.shape[3]
     if rows is not None:
         g = g.reshape(-1, D)[rows]
+        g_plain = g_plain.reshape(-1, D)[rows]
         ls = ls.reshape(-1, 2)[rows]
     else:
         ls = ls.reshape(L.shape + (2,))
-    assert_close(g, r, dtype, what)
+    assert_close(g_plain, r, dtype, what + " (plain)")
+    assert_close(g, r, dtype, what + " (with statistics)")
     # Eq. 4's statistics: L to fp32 rounding of the logits, S to the rounding of p
     assert np.max(np.abs(ls[..., 0] - L) / np.maximum(1.0, np.abs(L))) <= 1e-5, what
     srel = 2e-3 if dtype == "f16" else 1e-2
@@ -136,6 +141,17 @@ def test_statistics_output_does_not_change_o(Lk, D):
     o_plain = run_forward(q, k, v, scale)
     o_stats, _ = run_forward(q, k, v, scale, want_ls=True)
     assert np.array_equal(o_plain, o_stats)
+
+
+# Grids of at least 256 workgroups of 256 query rows take the largest
+# geometry (eight waves, 128-key tiles) for D <= 64: a partial last query
+# block, a ragged last key tile in either half, every head width it covers.
+@pytest.mark.parametrize("Lk,D", [(1000, 40), (1100, 32), (900, 48), (1000, 64), (4095, 40)])
+def test_large_grid_ragged(Lk, D):
+    q, k, v = wl.make_qkv(2, 8, 4000, Lk, D, 3700 + Lk + D)
+    rows = wl.sample_rows(2, 8, 4000, 16, seed=Lk + D)
+    rows = np.unique(np.concatenate([rows, [4000 * 16 - 1, 3999, 3840]]))
+    check_case(q, k, v, float(np.float32(1 / np.sqrt(D))), rows=rows, what=f"Lq=4000 Lk={Lk} D={D}")
 
 
 @pytest.mark.parametrize("scale", [0.0, -0.2, 1.0])

@@ -146,12 +146,14 @@ def test_statistics_output_does_not_change_o(Lk, D):
 # Grids of at least 256 workgroups of 256 query rows take the largest
 # geometry (eight waves, 128-key tiles) for D <= 64: a partial last query
 # block, a ragged last key tile in either half, every head width it covers.
-@pytest.mark.parametrize("Lk,D", [(1000, 40), (1100, 32), (900, 48), (1000, 64), (4095, 40)])
-def test_large_grid_ragged(Lk, D):
-    q, k, v = wl.make_qkv(2, 8, 4000, Lk, D, 3700 + Lk + D)
+@pytest.mark.parametrize("Lk,D,dtype", [(1000, 40, "f16"), (1100, 32, "f16"), (900, 48, "f16"),
+                                        (1000, 64, "f16"), (4095, 40, "f16"), (1000, 40, "bf16")])
+def test_large_grid_ragged(Lk, D, dtype):
+    q, k, v = wl.make_qkv(2, 8, 4000, Lk, D, 3700 + Lk + D, dtype=dtype)
     rows = wl.sample_rows(2, 8, 4000, 16, seed=Lk + D)
     rows = np.unique(np.concatenate([rows, [4000 * 16 - 1, 3999, 3840]]))
-    check_case(q, k, v, float(np.float32(1 / np.sqrt(D))), rows=rows, what=f"Lq=4000 Lk={Lk} D={D}")
+    check_case(q, k, v, float(np.float32(1 / np.sqrt(D))), dtype=dtype, rows=rows,
+               what=f"Lq=4000 Lk={Lk} D={D} {dtype}")
 
 
 @pytest.mark.parametrize("scale", [0.0, -0.2, 1.0])

@@ -17,7 +17,7 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libsdattn.so")
 ARCH = "gfx950"
 
-SOURCES = ["attn_fwd.hip", "attn_fwd_short.hip", "attn_fwd_generic.hip", "softmax_rows.hip",
+SOURCES = ["attn_fwd.hip", "attn_fwd_bf16.hip", "attn_fwd_short.hip", "attn_fwd_generic.hip", "softmax_rows.hip",
            "twopass.hip", "linear.hip", "norm_act.hip", "winograd.hip",
            "sdattn_api.hip"]
 

@@ -22,6 +22,8 @@ struct AttnArgs {
 long long attn_fwd_grid(int B, int H, int Lq);
 // Picks the kernel for (D, Lk) and launches it.
 hipError_t launch_attn_fwd(const AttnArgs& a);
+// the bf16 instantiations of the tiled kernel (a translation unit of their own)
+hipError_t launch_attn_fwd_tiled_bf16(const AttnArgs& a);
 // The generic kernel (any D % 8 == 0 up to 256).
 hipError_t launch_attn_fwd_generic(const AttnArgs& a);
 // The short-sequence kernel (all keys resident in LDS): Lk <= 128, 32 <= D <= 160.

@@ -7,7 +7,7 @@
 //
 // This is the method the paper uses where its FlashAttention kernel does not
 // pay off; the A matrix travels through HBM three times (written once, read
-// twice).  The single-pass kernel (attn_fwd.hip) never materialises it.
+// twice).  The single-pass kernel (attn_fwd_kernel.h) never materialises it.
 //
 // Both kernels use 32x32x16 MFMAs with one query per lane, as the fused
 // kernel does.

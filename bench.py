@@ -452,8 +452,14 @@ def cpu_baseline(wl, self_case, cross_case, rows_per_head):
     oracle.attention(cq, ck, cv, cross_case.scale, rows=crows)
     t_cross = time.perf_counter() - t0
     flops = 4 * (rows.size * self_case.Lk + crows.size * cross_case.Lk) * self_case.D
+    cpu = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
+    except OSError:
+        pass
     return {"value": round(flops / (t_self + t_cross) / 1e12, 8), "unit": "TFLOP/s",
-            "cores": oracle.num_threads(), "kind": "oracle",
+            "cores": oracle.num_threads(), "kind": "oracle", "cpu": cpu,
             "sample": f"{rows.size} self-attention rows and {crows.size} cross-attention rows of the step "
                       f"(fp64 three-pass, {t_self + t_cross:.1f} s)",
             "seconds": round(t_self + t_cross, 3)}

@@ -45,7 +45,7 @@ def _load():
         lib = ctypes.CDLL(_build.LIB)
         vp, i32, i64, f32 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_float
         lib.oracle_attention_f64.argtypes = [vp, vp, vp, i32, i32, i32, i32, i32, i32,
-                                             f32, vp, i64, i32, vp, vp, vp]
+                                             f32, vp, i64, i32, vp, vp, vp, vp]
         lib.oracle_attention_f64.restype = i32
         lib.oracle_softmax_rows_f64.argtypes = [vp, i32, i64, i64, f32, i32, vp, vp]
         lib.oracle_softmax_rows_f64.restype = i32
@@ -108,13 +108,16 @@ def widen(x, dtype=None):
     return out
 
 
-def attention(q, k, v, scale, rows=None, dtype=None, nthreads=0):
+def attention(q, k, v, scale, rows=None, dtype=None, nthreads=0, want_dev=False):
     """Eq. 3 in fp64.  q: [B,H,Lq,D], k, v: [B,H,Lk,D], same element type.
 
     rows: optional 1-D array of flat query-row indices (b*H + h)*Lq + i; the
     outputs then hold only those rows, in that order.
     Returns (O, L, S): O is [B,H,Lq,D] (or [len(rows), D]); L and S are
     Eq. 4's row maximum and shifted exponential sum, shaped like O[..., 0].
+    With want_dev, also DEV shaped like O: dev_id = sum_j p_ij |v_jd - o_id|,
+    the weighted mean absolute deviation of each value column (what a
+    relative rounding of the weights can move o_id by, to first order).
     """
     q, k, v = (np.ascontiguousarray(t) for t in (q, k, v))
     if q.ndim != 4 or k.shape != v.shape or q.shape[:2] != k.shape[:2] or q.shape[3] != k.shape[3]:
@@ -132,12 +135,13 @@ def attention(q, k, v, scale, rows=None, dtype=None, nthreads=0):
     out = np.empty(shape + (D,), dtype=np.float64)
     L = np.empty(shape, dtype=np.float64)
     S = np.empty(shape, dtype=np.float64)
+    dev = np.empty(shape + (D,), dtype=np.float64) if want_dev else None
     rc = _load().oracle_attention_f64(_ptr(q), _ptr(k), _ptr(v), code, B, H, Lq, Lk, D,
                                       float(np.float32(scale)), rp, n, int(nthreads),
-                                      _ptr(out), _ptr(L), _ptr(S))
+                                      _ptr(out), _ptr(L), _ptr(S), _ptr(dev) if want_dev else None)
     if rc != 0:
         raise ValueError("oracle_attention_f64 rejected its arguments")
-    return out, L, S
+    return (out, L, S, dev) if want_dev else (out, L, S)
 
 
 def softmax_rows(a, scale=1.0, want_p=False, dtype=None, nthreads=0):

@@ -108,12 +108,18 @@ int oracle_widen(const void *src, int dtype, int64_t n, double *dst)
  *       r = (b*H + h)*Lq + i selecting the rows to compute.
  * out:  [nrows or B*H*Lq][D] doubles, row by row in the order asked for.
  * L, S: optional [same rows] doubles receiving Eq. 4's L_i and S_i.
+ * dev:  optional [same rows][D] doubles receiving, after the three passes,
+ *       dev_id = sum_j p_ij |v_jd - o_id| with p_ij = exp(a_ij - L_i) / S_i:
+ *       the mean absolute deviation of the value column under the weights.
+ *       It is not part of Eq. 3; the GPU parity tests derive from it how far
+ *       a relative rounding of every weight can move o_id (first order: by at
+ *       most that relative size times dev_id).
  * Returns 0, or 1 on a bad argument.
  */
 int oracle_attention_f64(const void *q, const void *k, const void *v, int dtype,
                          int B, int H, int Lq, int Lk, int D, float scale,
                          const int64_t *rows, int64_t nrows, int nthreads,
-                         double *out, double *L, double *S)
+                         double *out, double *L, double *S, double *dev)
 {
     if (!q || !k || !v || !out || B < 1 || H < 1 || Lq < 1 || Lk < 1 || D < 1 ||
         dtype < OR_F16 || dtype > OR_F64)
@@ -165,6 +171,16 @@ int oracle_attention_f64(const void *q, const void *k, const void *v, int dtype,
                     const double pij = exp(a[j] - Li) / Si;
                     for (int d = 0; d < D; ++d)
                         o[d] += pij * or_elem(v, dtype, kv0 + (int64_t)j * D + d);
+                }
+                if (dev) {
+                    double *e = dev + t * D;
+                    for (int d = 0; d < D; ++d)
+                        e[d] = 0.0;
+                    for (int j = 0; j < Lk; ++j) {
+                        const double pij = exp(a[j] - Li) / Si;
+                        for (int d = 0; d < D; ++d)
+                            e[d] += pij * fabs(or_elem(v, dtype, kv0 + (int64_t)j * D + d) - o[d]);
+                    }
                 }
                 if (L)
                     L[t] = Li;

@@ -58,6 +58,7 @@ def _brute_force(q, k, v, scale):
     qf, kf, vf = (t.astype(np.float64) for t in (q, k, v))
     sc = mpmath.mpf(float(np.float32(scale)))
     out = np.zeros((B, H, Lq, D))
+    devs = np.zeros((B, H, Lq, D))
     Ls = np.zeros((B, H, Lq))
     Ss = np.zeros((B, H, Lq))
     for b in range(B):
@@ -68,11 +69,14 @@ def _brute_force(q, k, v, scale):
                 w = [mpmath.exp(x) for x in s]
                 tot = mpmath.fsum(w)
                 for d in range(D):
-                    out[b, h, i, d] = float(mpmath.fsum(w[j] * mpmath.mpf(float(vf[b, h, j, d]))
-                                                        for j in range(Lk)) / tot)
+                    od = mpmath.fsum(w[j] * mpmath.mpf(float(vf[b, h, j, d])) for j in range(Lk)) / tot
+                    out[b, h, i, d] = float(od)
+                    devs[b, h, i, d] = float(mpmath.fsum(
+                        w[j] * abs(mpmath.mpf(float(vf[b, h, j, d])) - od) for j in range(Lk)) / tot)
                 L = max(s)
                 Ls[b, h, i] = float(L)
                 Ss[b, h, i] = float(mpmath.fsum(mpmath.exp(x - L) for x in s))
+    _brute_force.dev = devs
     return out, Ls, Ss
 
 
@@ -97,12 +101,58 @@ def test_brute_force_small(shape):
     v = _rand16(rng, (B, H, Lk, D))
     if scale is None:
         scale = float(np.float32(1 / np.sqrt(D)))
-    o, L, S = oracle.attention(q, k, v, scale)
+    o, L, S, dev = oracle.attention(q, k, v, scale, want_dev=True)
     ro, rL, rS = _brute_force(q, k, v, scale)
     vmax = np.abs(v.astype(np.float64)).max()
     assert np.max(np.abs(o - ro)) <= 1e-12 * vmax
     assert np.max(np.abs(L - rL) / np.maximum(1.0, np.abs(rL))) <= 1e-12
     assert np.max(np.abs(S - rS) / rS) <= 1e-12
+    # the weighted mean absolute deviation of the value columns (the parity
+    # tests' sensitivity of O to a relative rounding of the weights)
+    assert np.max(np.abs(dev - _brute_force.dev)) <= 1e-12 * vmax
+    o2, L2, S2 = oracle.attention(q, k, v, scale)
+    assert np.array_equal(o, o2) and np.array_equal(L, L2) and np.array_equal(S, S2)
+
+
+def test_value_deviation_closed_forms():
+    """dev_id = sum_j p_ij |v_jd - o_id|: zero for one key or constant value
+    columns; |v_0 - v_1| / 2 for two keys of equal logit; bounded by the
+    largest |v_jd - o_id|; and, being first order in the weights, the change
+    of o_id when every weight is rounded by a relative 2^-11."""
+    rng = np.random.default_rng(12)
+    q = _rand16(rng, (1, 2, 9, 16), 2.0)
+    k = _rand16(rng, (1, 2, 1, 16))
+    v = _rand16(rng, (1, 2, 1, 16))
+    _, _, _, dev = oracle.attention(q, k, v, 0.3, want_dev=True)
+    assert np.all(dev == 0.0)
+    k = _rand16(rng, (1, 2, 13, 16))
+    v = np.broadcast_to(_rand16(rng, (1, 2, 1, 16)), (1, 2, 13, 16)).copy()
+    _, _, _, dev = oracle.attention(q, k, v, 0.3, want_dev=True)
+    assert np.max(np.abs(dev)) <= 1e-15
+    # two identical keys: equal weights
+    k = np.broadcast_to(_rand16(rng, (1, 2, 1, 16)), (1, 2, 2, 16)).copy()
+    v = _rand16(rng, (1, 2, 2, 16))
+    _, _, _, dev = oracle.attention(q, k, v, 0.3, want_dev=True)
+    vf = v.astype(np.float64)
+    half = np.abs(vf[:, :, 0] - vf[:, :, 1])[:, :, None, :] / 2
+    assert np.max(np.abs(dev - np.broadcast_to(half, dev.shape))) <= 1e-15
+    # bound and first-order sensitivity on random inputs
+    q = _rand16(rng, (1, 1, 7, 16), 2.0)
+    k = _rand16(rng, (1, 1, 50, 16))
+    v = _rand16(rng, (1, 1, 50, 16))
+    o, L, S, dev = oracle.attention(q, k, v, 0.4, want_dev=True)
+    vf = v.astype(np.float64)[0, 0]
+    assert np.all(dev[0, 0] <= np.abs(vf[None, :, :] - o[0, 0][:, None, :]).max(axis=1) + 1e-15)
+    a = oracle.logits(q, k, 0.4)[0, 0]
+    p = np.exp(a - L[0, 0][:, None]) / S[0, 0][:, None]
+    worst = 0.0
+    for trial in range(200):
+        delta = rng.choice([-1.0, 1.0], size=p.shape) * 2.0 ** -11
+        pt = p * (1 + delta)
+        ot = (pt @ vf) / pt.sum(axis=1, keepdims=True)
+        worst = max(worst, float(np.max(np.abs(ot - o[0, 0]) / (2.0 ** -11 * dev[0, 0] * (1 + 2.0 ** -10)
+                                                                   + 1e-300))))
+    assert worst <= 1.0
 
 
 # --------------------------------------------------------------- structure

@@ -16,3 +16,13 @@ def pytest_configure(config):
 def gpu_available():
     import torch
     return torch.cuda.is_available()
+
+
+def pytest_sessionfinish(session, exitstatus):
+    # per-call parity statistics (max |g - r|, elements above the flat bound),
+    # written only when SDATTN_PARITY_REPORT names a file
+    try:
+        import parity_util
+    except ImportError:
+        return
+    parity_util.write_report()

@@ -46,15 +46,6 @@ constexpr float kRescaleSlack = 8.0f;
 // the 16-byte reads of 16 consecutive rows on distinct LDS banks.
 __host__ __device__ constexpr int k_pitch(int D) { return ((D / 8) & 1) ? D : D + 8; }
 
-// Logical tile for workgroup `bid`.  Workgroups are dealt round-robin over the
-// 8 XCDs; give every XCD a contiguous run of logical tiles so that the tiles
-// of one (batch, head) -- which read the same K and V -- share one L2.
-__device__ __forceinline__ int xcd_remap(int bid, int nblk) {
-    const int per = nblk / 8, rem = nblk % 8;
-    const int xcd = bid % 8, slot = bid / 8;
-    return xcd < rem ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
-}
-
 template <int ET, int DK>
 __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ K, const uint16_t* __restrict__ V,

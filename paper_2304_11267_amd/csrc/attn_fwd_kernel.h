@@ -71,10 +71,6 @@ constexpr int kGeoBig = 2;             // 256 rows, 128-key tiles (QB = 2 only)
 constexpr float kRescaleSlack = 8.0f;
 constexpr int kMaxLds = 160 * 1024;
 
-typedef short s16x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) void lds_void_t;
-typedef __attribute__((address_space(3))) s16x4 lds_s16x4_t;
-
 // QB = 32-row query blocks per wave.  With QB = 2 every K and V^T operand
 // read from LDS feeds two MFMAs (half the LDS traffic per flop) and each wave
 // carries two independent MFMA / softmax chains; the register budget is then
@@ -113,20 +109,6 @@ struct Geom {
     static constexpr int kWgPerCu = kLdsBytes <= kMaxLds ? kMaxLds / kLdsBytes : 1;
     static constexpr int kWavesPerSimd = kWgPerCu * kWaves >= 8 ? 2 : 1;
 };
-
-// Logical tile for workgroup `bid`.  Workgroups are dealt round-robin over the
-// 8 XCDs; give every XCD a contiguous run of logical tiles so that the tiles
-// of one (batch, head) -- which read the same K and V -- share one L2.
-__device__ __forceinline__ int xcd_remap(int bid, int nblk) {
-    const int per = nblk / 8, rem = nblk % 8;
-    const int xcd = bid % 8, slot = bid / 8;
-    return xcd < rem ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
-}
-
-__device__ __forceinline__ u32x2 lds_read_tr(const char* p) {
-    const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)p);
-    return __builtin_bit_cast(u32x2, v);
-}
 
 template <int ET, int D, bool STATS, bool OROWS, int GEO>
 __global__ __launch_bounds__((Geom<D, GEO>::kThreads), (Geom<D, GEO>::kWavesPerSimd)) void attn_fwd_lds_kernel(
@@ -560,6 +542,11 @@ __global__ __launch_bounds__((Geom<D, GEO>::kThreads), (Geom<D, GEO>::kWavesPerS
         if (any) {
             reset();
             run_tiles(online_c);
+            // The merge below writes into the tile buffers; a wave of key
+            // half 1 may still be reading its ragged last tile there (run_tiles
+            // ends without a barrier after that tile).  The fixed-maximum pass
+            // has the vote's barriers in between.
+            __syncthreads();
         }
     }
 

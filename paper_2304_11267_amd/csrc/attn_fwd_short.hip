@@ -34,11 +34,6 @@ namespace sdattn {
 
 namespace {
 
-
-typedef short s16x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) void lds_void_t;
-typedef __attribute__((address_space(3))) s16x4 lds_s16x4_t;
-
 template <int D, int NS, int W>
 struct ShortGeom {
     static constexpr int DK = (D + 15) / 16;
@@ -56,17 +51,6 @@ struct ShortGeom {
     static constexpr bool kFits = kLdsBytes <= 160 * 1024;
     static_assert(kBlockBytes % 16 == 0 && kStripBytes % 16 == 0, "16-byte LDS chunks");
 };
-
-__device__ __forceinline__ int xcd_remap(int bid, int nblk) {
-    const int per = nblk / 8, rem = nblk % 8;
-    const int xcd = bid % 8, slot = bid / 8;
-    return xcd < rem ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
-}
-
-__device__ __forceinline__ u32x2 lds_read_tr(const char* p) {
-    const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)p);
-    return __builtin_bit_cast(u32x2, v);
-}
 
 // Arguments used first come first, so they fit in the preloaded kernel-argument
 // registers.

@@ -121,6 +121,31 @@ __device__ __forceinline__ float half_partner(float x, int half) {
 
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
 
+// 16-bit element groups for the transposing LDS read, and LDS address-space
+// pointer types for the builtins that take them.
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4_t;
+
+// Logical tile for workgroup `bid` of `nblk`.  Workgroups are dealt
+// round-robin over the 8 XCDs; this gives every XCD a contiguous run of
+// logical tiles, so that tiles which read the same operands (the query blocks
+// of one (batch, head), or the token tiles of one weight slice) share one L2.
+__device__ __forceinline__ int xcd_remap(int bid, int nblk) {
+    const int per = nblk / 8, rem = nblk % 8;
+    const int xcd = bid % 8, slot = bid / 8;
+    return xcd < rem ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
+}
+
+// ds_read_b64_tr_b16: within each group of 16 lanes, lane i receives the
+// 16-bit element i % 4 of the 8 bytes that lanes i / 4 + {0, 4, 8, 12} point
+// at -- four consecutive rows of one column of a row-major tile when each
+// lane points at four consecutive columns of one row.
+__device__ __forceinline__ u32x2 lds_read_tr(const char* p) {
+    const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)p);
+    return __builtin_bit_cast(u32x2, v);
+}
+
 // Where query row i of head bh = b*H + h goes in O: out_base(O, ...) + i * out_stride.
 // oh == 0: O is [B, H, Lq, D]; oh == H: O is [B, Lq, H*D] (the heads merged
 // into token rows).

@@ -33,7 +33,6 @@ namespace sdattn {
 
 namespace {
 
-typedef __attribute__((address_space(3))) void lds_void_t;
 
 constexpr int kBM = 128;                          // token rows per workgroup
 constexpr int kBN = 64;                           // output channels per workgroup
@@ -59,12 +58,6 @@ struct LinGroup {
     LinProblem p[kMaxLinearProblems];
     int n;
 };
-
-__device__ __forceinline__ int xcd_remap(int bid, int nblk) {
-    const int per = nblk / 8, rem = nblk % 8;
-    const int xcd = bid % 8, slot = bid / 8;
-    return xcd < rem ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
-}
 
 // chunk-position swizzle of row r: distinct for any 8 consecutive rows, and
 // (r & 1, swz) distinct for any 16 consecutive rows

@@ -18,25 +18,11 @@ namespace sdattn {
 
 namespace {
 
-typedef short s16x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) void lds_void_t;
-typedef __attribute__((address_space(3))) s16x4 lds_s16x4_t;
 
 constexpr int kLgQ = 128;   // logits tile: query rows (4 waves x 32)
 constexpr int kLgK = 128;   // logits tile: keys
 constexpr int kPvQ = 128;   // softmax_pv: query rows per workgroup (4 waves x 32)
 constexpr int kPvK = 64;    // softmax_pv: keys per V tile
-
-__device__ __forceinline__ int xcd_remap(int bid, int nblk) {
-    const int per = nblk / 8, rem = nblk % 8;
-    const int xcd = bid % 8, slot = bid / 8;
-    return xcd < rem ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
-}
-
-__device__ __forceinline__ u32x2 lds_read_tr(const char* p) {
-    const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)p);
-    return __builtin_bit_cast(u32x2, v);
-}
 
 template <int OT>
 constexpr int out_size() { return OT == kF32 ? 4 : 2; }

@@ -73,11 +73,21 @@ def test_linear_matches_oracle(shape, mode):
     use_bias = mode.endswith("bias")
     x_heads = mode.startswith("heads")
     y_heads = mode == "rows_heads"
-    if (x_heads and (K % H or (K // H) % 8)) or (y_heads and (N % H or (N // H) % 8)):
-        pytest.skip("head width not a multiple of 8")
     xd = to_device(heads_of(x, H) if x_heads else x)
     wd, bd = to_device(w), to_device(bias)
     y = torch.empty((B, H, L, N // H) if y_heads else (B, L, N), dtype=torch.float16, device="cuda")
+    if (x_heads and (K % H or (K // H) % 8)) or (y_heads and (N % H or (N // H) % 8)):
+        # a head width that is not a multiple of 8 is refused before any launch,
+        # and y is left as it was
+        y.fill_(7.0)
+        with pytest.raises(sd.SdattnError) as e:
+            sd.linear(xd, wd, y, bias=bd if use_bias else None, heads=H,
+                      x_layout=sd.LAYOUT_HEADS if x_heads else sd.LAYOUT_ROWS,
+                      y_layout=sd.LAYOUT_HEADS if y_heads else sd.LAYOUT_ROWS)
+        assert e.value.status == sd.STATUS_UNSUPPORTED
+        torch.cuda.synchronize()
+        assert bool((y == 7.0).all())
+        return
     sd.linear(xd, wd, y, bias=bd if use_bias else None, heads=H,
               x_layout=sd.LAYOUT_HEADS if x_heads else sd.LAYOUT_ROWS,
               y_layout=sd.LAYOUT_HEADS if y_heads else sd.LAYOUT_ROWS)

@@ -16,6 +16,14 @@ Also reported, on the same stream with HIP events:
   softmax_rows  Eq. 4's row reduction over A = Q K^T of the 64x64 level
                 (65536 rows x 4096 fp16), which the fused kernels never
                 materialise; timed alone, not part of the step
+  sweep         one UNet evaluation (16 blocks, self- then cross-attention)
+                per denoising step over 20 steps with per-step inputs, and
+                each level's kernels against their rooflines
+  peaks_measured  what the chip sustains, from the measurement kernels of
+                libsdattn_probes.so: fp16 MFMA rate and shader clock under
+                that load, v_exp_f32 / v_fma_f32 rates and their overlap with
+                the matrix core, HBM streaming, and a plain copy with the
+                cross-attention kernel's grid and bytes (cold)
   cpu_baseline  the fp64 oracle on a bounded row sample of the same step
 """
 import argparse
@@ -43,10 +51,12 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing")
     ap.add_argument("--no-extras", action="store_true",
                     help="time only the step (no cold cross or softmax_rows legs)")
-    ap.add_argument("--cpu-rows-per-head", type=int, default=5120,
+    ap.add_argument("--cpu-rows-per-head", type=int, default=1536,
                     help="self-attention rows per (b, h) the oracle times")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 256 MiB device copy (scales the HBM traffic counters)")
+    ap.add_argument("--no-sweep", action="store_true", help="skip the 20-step UNet sweep")
+    ap.add_argument("--no-probes", action="store_true", help="skip the measured-peak probes")
     return ap.parse_args()
 
 
@@ -161,6 +171,22 @@ def main():
                                              {"self": self_ms, "cross": warm_ms})
         out["norm_act"] = bench_norm_act(torch, sd, wl, dev, stream)
         out["conv3x3_winograd"] = bench_conv(torch, sd, wl, dev, stream)
+
+    if not args.no_probes:
+        peaks = measured_peaks(torch, dev, stream)
+        out["peaks_measured"] = peaks
+        mp = peaks["mfma_f16_tflops"]
+        roofline["peak_measured"] = mp
+        roofline["frac_measured"] = round(self_tflops / mp, 4)
+        hp = peaks["hbm_copy_gbs"]
+        out["cross"]["peak_measured_gbs"] = hp
+        out["cross"]["warm_frac_measured"] = round(cross_gbs / hp, 4)
+        if "cold_gbs" in out["cross"]:
+            out["cross"]["cold_frac_measured"] = round(out["cross"]["cold_gbs"] / hp, 4)
+        out["cross"]["floor"] = cross_floor(torch, wl, dev, stream, cross_case)
+
+    if not args.no_sweep:
+        out["sweep"] = bench_sweep(torch, sd, wl, dev, stream)
 
     if args.copy_calibration:
         out["copy_calibration"] = copy_calibration(torch, dev, stream)
@@ -404,6 +430,184 @@ def bench_conv(torch, sd, wl, dev, stream, launches=30, reps=3):
             "shape": f"x [{B},{C},{L},{L}] w [{C},{C},3,3]"}
 
 
+def _events_ms(torch, stream, call, reps=3):
+    """Best of `reps` single timed calls (after one untimed call), events on `stream`."""
+    call()
+    torch.cuda.synchronize()
+    best = None
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        call()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        best = ms if best is None else min(best, ms)
+    return best
+
+
+def measured_peaks(torch, dev, stream):
+    """Sustained rates from the measurement kernels (libsdattn_probes.so).
+
+    mfma_f16_tflops    back-to-back v_mfma_f32_32x32x16_f16, two waves per SIMD
+    shader_clock_ghz   the shader-clock counter against the 100 MHz counter
+                       during that stream (clock under matrix-core load)
+    exp / fma          wave64 instructions per SIMD per shader cycle, alone
+    overlap_*          time of one MFMA wave + one VALU wave per SIMD against
+                       each alone: 0 = the sum of both (no overlap), 1 = the
+                       longer of the two (full overlap)
+    hbm_*_gbs          1 GiB copy (read + write bytes / time) and 2 GiB read
+    """
+    from paper_2304_11267_amd import probes
+    blocks = 512                                   # 2 workgroups of 8 waves per CU
+    out = torch.empty(blocks * 512, dtype=torch.float32, device=dev)
+    clk = torch.zeros(4, dtype=torch.int64, device=dev)
+    it_m, it_v = 8000, 8000
+
+    def run(mode, im, iv, c=None):
+        return _events_ms(torch, stream, lambda: probes.mix(mode, blocks, im, iv, out, c, stream))
+
+    t_mfma = run(probes.MIX_MFMA, it_m, 0, clk)
+    torch.cuda.synchronize()
+    t0, t1, r0, r1 = (int(x) for x in clk.cpu().tolist())
+    clock_ghz = (t1 - t0) / ((r1 - r0) / 100e6) / 1e9 if r1 > r0 else None
+    mfma_tf = blocks * 8 * it_m * probes.MFMA_FLOPS_PER_ITER / (t_mfma * 1e-3) / 1e12
+    t_fma = run(probes.MIX_FMA, 0, it_v)
+    t_exp = run(probes.MIX_EXP, 0, it_v // 2)
+    simds = 256 * 4
+    waves_per_simd = blocks * 8 / simds
+    res = {"mfma_f16_tflops": round(mfma_tf, 1),
+           "mfma_f16_frac_of_datasheet": round(mfma_tf / PEAK_F16_TFLOPS, 4),
+           "shader_clock_ghz": round(clock_ghz, 3) if clock_ghz else None}
+    if clock_ghz:
+        cyc = lambda ms: ms * 1e-3 * clock_ghz * 1e9
+        res["fma_cycles_per_wave64_op"] = round(cyc(t_fma) / (waves_per_simd * it_v * 16), 2)
+        res["exp_cycles_per_wave64_op"] = round(cyc(t_exp) / (waves_per_simd * (it_v // 2) * 16), 2)
+        res["mfma32x32x16_cycles"] = round(cyc(t_mfma) / (waves_per_simd * it_m * 4), 2)
+    # one MFMA wave and one VALU wave per SIMD (waves 0-3 and 4-7 of each workgroup)
+    half_m = run(probes.MIX_MFMA_HALF, it_m // 2, 0)
+    for name, both_mode, alone_mode, iv in (("fma", probes.MIX_MFMA_FMA, probes.MIX_FMA_HALF, it_v),
+                                            ("exp", probes.MIX_MFMA_EXP, probes.MIX_EXP_HALF, it_v // 2)):
+        alone_v = run(alone_mode, 0, iv)
+        both = run(both_mode, it_m // 2, iv)
+        lo, hi = max(half_m, alone_v), half_m + alone_v
+        res[f"overlap_mfma_{name}"] = round((hi - both) / (hi - lo), 3) if hi > lo else None
+        res[f"mfma_{name}_us"] = {"mfma_alone": round(half_m * 1e3, 1), f"{name}_alone": round(alone_v * 1e3, 1),
+                                  "together": round(both * 1e3, 1)}
+    # HBM streaming (buffers far beyond the 256 MB Infinity Cache)
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device=dev)
+    dst = torch.empty(n, dtype=torch.uint8, device=dev)
+    src.fill_(1)
+    cblocks = 256 * 32
+    t_copy = _events_ms(torch, stream, lambda: probes.copy(src, dst, n, cblocks, stream))
+    big = torch.empty(2 * n, dtype=torch.uint8, device=dev)
+    big.fill_(3)
+    sink = torch.empty(cblocks * 256, dtype=torch.int32, device=dev)
+    t_read = _events_ms(torch, stream, lambda: probes.read(big, 2 * n, sink, cblocks, stream))
+    res["hbm_copy_gbs"] = round(2 * n / (t_copy * 1e-3) / 1e9, 1)
+    res["hbm_read_gbs"] = round(2 * n / (t_read * 1e-3) / 1e9, 1)
+    res["hbm_copy_frac_of_datasheet"] = round(res["hbm_copy_gbs"] / PEAK_HBM_GBS, 4)
+    del src, dst, big
+    return res
+
+
+def cross_floor(torch, wl, dev, stream, case, nsets=40):
+    """The cross-attention kernel's bytes moved by a plain copy with its grid
+    (256-row workgroups of eight waves, each reading its head's K and V and
+    copying its Q rows to O), inputs rotated over `nsets` sets as in the cold
+    protocol: the floor for any kernel that moves those bytes that way."""
+    from paper_2304_11267_amd import probes
+    sets = []
+    g = torch.Generator(device=dev)
+    g.manual_seed(case.seed)
+    for _ in range(nsets):
+        q = torch.randn(case.B, case.H, case.Lq, case.D, device=dev, generator=g).half()
+        k = torch.randn(case.B, case.H, case.Lk, case.D, device=dev, generator=g).half()
+        v = torch.randn(case.B, case.H, case.Lk, case.D, device=dev, generator=g).half()
+        sets.append((q, k, v, torch.empty_like(q)))
+    sink = torch.empty(case.B * case.H * ((case.Lq + 255) // 256), dtype=torch.int32, device=dev)
+    launches = 5 * nsets
+
+    def batch(rot):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(20_000_000)
+        e0.record(stream)
+        for i in range(launches):
+            s = sets[i % nsets] if rot else sets[0]
+            probes.strip_copy(*s, sink, stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / launches
+
+    for s in sets:
+        probes.strip_copy(*s, sink, stream)
+    torch.cuda.synchronize()
+    cold = min(batch(True) for _ in range(3))
+    warm = min(batch(False) for _ in range(3))
+    return {"cold_us": round(cold * 1e3, 3), "cold_gbs": round(case.bytes / (cold * 1e-3) / 1e9, 1),
+            "warm_us": round(warm * 1e3, 3), "warm_gbs": round(case.bytes / (warm * 1e-3) / 1e9, 1),
+            "what": "plain copy of Q to O plus reads of K, V with the cross kernel's grid, "
+                    f"{nsets} rotated input sets (cold) or one (warm), back-to-back launches"}
+
+
+def bench_sweep(torch, sd, wl, dev, stream, steps=20, launches=20):
+    """Config 5: the 32 attention calls of one UNet evaluation (16 blocks,
+    self- then cross-attention) at each of 20 denoising steps, every call on
+    its own inputs (N(0,1) drawn on the GPU from that call's seed; the timing
+    does not depend on the values on the fast path).  Reported: ms per UNet
+    evaluation over the 20 steps (one event pair around all 640 calls), and
+    per level and kind the average kernel time from back-to-back launches
+    with its roofline fraction."""
+    calls = []
+    for t in range(steps):
+        for case in wl.sweep_cases(t):
+            g = torch.Generator(device=dev)
+            g.manual_seed(case.seed)
+            q = torch.randn(case.B, case.H, case.Lq, case.D, device=dev, generator=g).half()
+            k = torch.randn(case.B, case.H, case.Lk, case.D, device=dev, generator=g).half()
+            v = torch.randn(case.B, case.H, case.Lk, case.D, device=dev, generator=g).half()
+            calls.append((case, (q, k, v, torch.empty_like(q))))
+    for case, s in calls[:32]:
+        sd.forward(*s, case.scale, stream)
+    torch.cuda.synchronize()
+    best = None
+    for _ in range(3):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(20_000_000)
+        e0.record(stream)
+        for case, s in calls:
+            sd.forward(*s, case.scale, stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        best = ms if best is None else min(best, ms)
+    per_eval_ms = best / steps
+    flops_per_eval = sum(c.flops for c, _ in calls[:32])
+    bytes_per_eval = sum(c.bytes for c, _ in calls[:32])
+    levels = {}
+    for level, (L, D) in sorted(wl.LEVELS.items(), reverse=True):
+        for kind in ("self", "cross"):
+            sel = [(c, s) for c, s in calls if c.Lq == L and c.D == D and c.name.endswith(kind)][:8]
+            ms = back_to_back_ms(torch, sd, stream, [s for _, s in sel], sel[0][0].scale, launches=launches)
+            c = sel[0][0]
+            tf = c.flops / (ms * 1e-3) / 1e12
+            gbs = c.bytes / (ms * 1e-3) / 1e9
+            levels[f"{level}x{level}_{kind}"] = {
+                "us": round(ms * 1e3, 2), "tflops": round(tf, 1), "frac_f16_peak": round(tf / PEAK_F16_TFLOPS, 4),
+                "gbs": round(gbs, 1), "frac_hbm": round(gbs / PEAK_HBM_GBS, 4),
+                "calls_per_eval": sum(1 for cc, _ in calls[:32] if cc.Lq == L and cc.D == D
+                                      and cc.name.endswith(kind)),
+                "shape": f"B{c.B} H{c.H} Lq{c.Lq} Lk{c.Lk} D{c.D}"}
+    del calls
+    return {"ms_per_unet_eval": round(per_eval_ms, 4), "steps": steps, "calls_per_eval": 32,
+            "flops_per_eval": flops_per_eval, "bytes_per_eval": bytes_per_eval,
+            "tflops": round(flops_per_eval / (per_eval_ms * 1e-3) / 1e12, 1),
+            "levels": levels,
+            "inputs": "per call N(0,1) fp16 from torch's GPU generator seeded with the call's seed "
+                      "(S0 + 1000(t+1) + 10b, +1 for cross)"}
+
+
 def copy_calibration(torch, dev, stream, nbytes=256 << 20, reps=3):
     """A plain device copy of known size: its FETCH_SIZE / WRITE_SIZE counter
     readings give the scale between those counters and bytes moved."""
@@ -440,29 +644,48 @@ def recorded_traffic():
 
 
 def cpu_baseline(wl, self_case, cross_case, rows_per_head):
+    """The fp64 oracle timed on this host: a bounded row sample of the step
+    (median of 3 runs) on every core the process may use, plus configs 1 and
+    2 (the 8x8 and 16x16 self-attention) whole on all cores and on one."""
     import oracle
+    cores = len(os.sched_getaffinity(0))
     q, k, v = wl.case_inputs(self_case)
     rows = wl.sample_rows(self_case.B, self_case.H, self_case.Lq, rows_per_head, seed=1)
-    t0 = time.perf_counter()
-    oracle.attention(q, k, v, self_case.scale, rows=rows)
-    t_self = time.perf_counter() - t0
     cq, ck, cv = wl.case_inputs(cross_case)
     crows = wl.sample_rows(cross_case.B, cross_case.H, cross_case.Lq, cross_case.Lq, seed=2)
-    t0 = time.perf_counter()
-    oracle.attention(cq, ck, cv, cross_case.scale, rows=crows)
-    t_cross = time.perf_counter() - t0
+    runs = []
+    for _ in range(3):
+        t0 = time.perf_counter()
+        oracle.attention(q, k, v, self_case.scale, rows=rows, nthreads=cores)
+        oracle.attention(cq, ck, cv, cross_case.scale, rows=crows, nthreads=cores)
+        runs.append(time.perf_counter() - t0)
+    t = float(np.median(runs))
     flops = 4 * (rows.size * self_case.Lk + crows.size * cross_case.Lk) * self_case.D
+    small = {}
+    for name in ("mid8_self", "l16_self"):
+        case = wl.CASES[name]
+        qq, kk, vv = wl.case_inputs(case)
+        for n in (cores, 1):
+            ts = []
+            for _ in range(3):
+                t0 = time.perf_counter()
+                oracle.attention(qq, kk, vv, case.scale, nthreads=n)
+                ts.append(time.perf_counter() - t0)
+            small[f"{name}_{'all' if n == cores else 1}_cores"] = {
+                "seconds": round(float(np.median(ts)), 4),
+                "gflops": round(case.flops / float(np.median(ts)) / 1e9, 3), "threads": n}
     cpu = ""
     try:
         with open("/proc/cpuinfo") as f:
             cpu = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
     except OSError:
         pass
-    return {"value": round(flops / (t_self + t_cross) / 1e12, 8), "unit": "TFLOP/s",
-            "cores": oracle.num_threads(), "kind": "oracle", "cpu": cpu,
+    return {"value": round(flops / t / 1e12, 8), "unit": "TFLOP/s",
+            "cores": cores, "kind": "oracle", "cpu": cpu,
             "sample": f"{rows.size} self-attention rows and {crows.size} cross-attention rows of the step "
-                      f"(fp64 three-pass, {t_self + t_cross:.1f} s)",
-            "seconds": round(t_self + t_cross, 3)}
+                      f"(fp64 three-pass on {cores} threads, median of 3 runs of {t:.1f} s)",
+            "seconds": round(t, 3), "runs_s": [round(x, 3) for x in runs],
+            "configs_1_2": small}
 
 
 if __name__ == "__main__":

@@ -1,7 +1,9 @@
 """Build libsdattn.so (the C ABI of include/sdattn.h) for gfx950 with hipcc.
 
 Each csrc/*.hip file is compiled separately (in parallel) and linked into a
-shared library in the package directory, where the binding loads it.
+shared library in the package directory, where the binding loads it.  The
+measurement kernels of include/sdattn_probes.h (csrc/probes.hip) go into a
+library of their own, libsdattn_probes.so, which only the benchmark loads.
 """
 from __future__ import annotations
 
@@ -15,6 +17,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libsdattn.so")
+PROBES_LIB = os.path.join(HERE, "libsdattn_probes.so")
+PROBE_SOURCES = ["probes.hip"]
 ARCH = "gfx950"
 
 SOURCES = ["attn_fwd.hip", "attn_fwd_bf16.hip", "attn_fwd_short.hip", "attn_fwd_generic.hip", "softmax_rows.hip",
@@ -56,16 +60,22 @@ def _compile(src: str, verbose: bool) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD, exist_ok=True)
-    with concurrent.futures.ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
-    tmp = LIB + ".tmp"
+def _link(objs, lib, verbose):
+    tmp = lib + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
+
+
+def build(verbose: bool = False) -> str:
+    os.makedirs(BUILD, exist_ok=True)
+    srcs = SOURCES + PROBE_SOURCES
+    with concurrent.futures.ThreadPoolExecutor(max_workers=len(srcs)) as ex:
+        objs = list(ex.map(lambda s: _compile(s, verbose), srcs))
+    _link(objs[:len(SOURCES)], LIB, verbose)
+    _link(objs[len(SOURCES):], PROBES_LIB, verbose)
     return LIB
 
 

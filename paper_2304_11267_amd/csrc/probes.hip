@@ -1,0 +1,198 @@
+// probes.hip -- measurement kernels (libsdattn_probes.so, include/sdattn_probes.h).
+//
+// They compute nothing of the attention.  The benchmark runs them to report
+// what the chip sustains beside its published peaks: the fp16 matrix-core
+// rate and the shader clock under that load, the v_exp_f32 and v_fma_f32
+// rates and whether each runs while the matrix core of the same SIMD is busy,
+// HBM streaming rates, and a plain copy with the cross-attention kernel's
+// grid and byte pattern (the floor for a kernel that moves those bytes).
+// Every loop is bounded by its arguments and every access is inside the
+// caller's buffers.
+#include "device.h"
+#include "sdattn_probes.h"
+
+namespace sdattn {
+namespace {
+
+// Four independent 32x32x16 f16 accumulators: back-to-back matrix-core work.
+__device__ __forceinline__ float mfma_stream(int iters) {
+    f16x8 a, b;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        a[i] = (_Float16)((threadIdx.x & 63) * 0.001f);
+        b[i] = (_Float16)0.5f;
+    }
+    f32x16 c0 = {}, c1 = {}, c2 = {}, c3 = {};
+    for (int it = 0; it < iters; ++it) {
+        c0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c0, 0, 0, 0);
+        c1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c1, 0, 0, 0);
+        c2 = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c2, 0, 0, 0);
+        c3 = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c3, 0, 0, 0);
+    }
+    float s = 0.0f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s += c0[r] + c1[r] + c2[r] + c3[r];
+    return s;
+}
+
+// 16 independent chains of one VALU operation: 0 = v_fma_f32, 1 = v_exp_f32.
+template <int OP>
+__device__ __forceinline__ float valu_stream(int iters) {
+    float f[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) f[i] = 0.25f + 0.001f * (float)((threadIdx.x & 63) + i);
+    for (int it = 0; it < iters; ++it) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            if constexpr (OP == 0) f[i] = fmaf(f[i], 0.999f, 0.0001f);
+            else f[i] = __builtin_amdgcn_exp2f(-f[i]);   // stays in [0.5, 1]
+        }
+    }
+    float s = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) s += f[i];
+    return s;
+}
+
+__global__ __launch_bounds__(512) void mix_kernel(float* __restrict__ out, int mode, int it_m, int it_v,
+                                                  unsigned long long* __restrict__ clk) {
+    const int wave = threadIdx.x >> 6;
+    const bool first = blockIdx.x == 0 && wave == 0;
+    unsigned long long t0 = 0, r0 = 0;
+    if (first) {
+        t0 = __builtin_amdgcn_s_memtime();
+        r0 = __builtin_amdgcn_s_memrealtime();
+    }
+    const bool low = wave < 4;   // waves 0-3: one per SIMD; 4-7: the second of each SIMD
+    float s = 0.0f;
+    switch (mode) {
+        case 0: s = mfma_stream(it_m); break;
+        case 1: s = valu_stream<0>(it_v); break;
+        case 2: s = valu_stream<1>(it_v); break;
+        case 3: s = low ? mfma_stream(it_m) : valu_stream<0>(it_v); break;
+        case 4: s = low ? mfma_stream(it_m) : valu_stream<1>(it_v); break;
+        case 5: s = low ? mfma_stream(it_m) : 0.0f; break;
+        case 6: s = low ? 0.0f : valu_stream<0>(it_v); break;
+        default: s = low ? 0.0f : valu_stream<1>(it_v); break;
+    }
+    out[(size_t)blockIdx.x * 512 + threadIdx.x] = s;
+    if (first && clk && (threadIdx.x & 63) == 0) {
+        const unsigned long long t1 = __builtin_amdgcn_s_memtime();
+        const unsigned long long r1 = __builtin_amdgcn_s_memrealtime();
+        clk[0] = t0;
+        clk[1] = t1;
+        clk[2] = r0;
+        clk[3] = r1;
+    }
+}
+
+__global__ __launch_bounds__(256) void copy_kernel(const u32x4* __restrict__ src, u32x4* __restrict__ dst,
+                                                   long long n) {
+    const long long stride = (long long)gridDim.x * blockDim.x;
+    for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) dst[i] = src[i];
+}
+
+__global__ __launch_bounds__(256) void read_kernel(const u32x4* __restrict__ src, long long n,
+                                                   unsigned* __restrict__ sink) {
+    const long long stride = (long long)gridDim.x * blockDim.x;
+    u32x4 x = {0u, 0u, 0u, 0u};
+    for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) x ^= src[i];
+    sink[(size_t)blockIdx.x * blockDim.x + threadIdx.x] = x[0] ^ x[1] ^ x[2] ^ x[3];
+}
+
+// Eight waves per workgroup, 256 query rows of one head: the data movement of
+// the short-sequence attention kernel's large-grid launch without its
+// arithmetic.  K and V (all Lk rows) and each wave's 32 query rows go
+// global -> LDS with 16-byte direct copies, all issued before any wait; after
+// the workgroup's barrier each wave stores its rows back out as O with
+// 16-byte lanes, as the kernel's epilogue does.
+__global__ __launch_bounds__(512) void strip_copy_kernel(const char* __restrict__ Q, const char* __restrict__ K,
+                                                         const char* __restrict__ V, char* __restrict__ O,
+                                                         unsigned* __restrict__ sink, int Lq, int Lk, int D,
+                                                         int nqb, int kv_span) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    const int tile = xcd_remap(blockIdx.x, gridDim.x);
+    const int bh = tile / nqb;
+    const int qb = tile - bh * nqb;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int kv_bytes = Lk * D * 2;                 // <= kv_span, a multiple of 1024
+    const char* kh = K + (size_t)bh * kv_bytes;
+    const char* vh = V + (size_t)bh * kv_bytes;
+    const int nkv = kv_span / 1024;
+    for (int c = wave; c < 2 * nkv; c += 8) {
+        const bool isv = c >= nkv;
+        const int cc = isv ? c - nkv : c;
+        const int byte = cc * 1024 + lane * 16;
+        if (byte < kv_bytes)
+            __builtin_amdgcn_global_load_lds((isv ? vh : kh) + byte,
+                                             (lds_void_t*)(smem + (isv ? kv_span : 0) + cc * 1024), 16, 0, 0);
+    }
+    const int strip = 32 * D * 2;
+    const int q0 = qb * 256 + wave * 32;
+    const int bytes = max(0, min(32, Lq - q0)) * D * 2;
+    char* stage = smem + 2 * kv_span + wave * strip;
+    const char* qs = Q + ((size_t)bh * Lq + max(q0, 0)) * D * 2;
+    for (int c = 0; c * 1024 < bytes; ++c) {
+        const int byte = c * 1024 + lane * 16;
+        if (byte < bytes) __builtin_amdgcn_global_load_lds(qs + byte, (lds_void_t*)(stage + c * 1024), 16, 0, 0);
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    char* os = O + ((size_t)bh * Lq + max(q0, 0)) * D * 2;
+    for (int b = lane * 16; b < bytes; b += 1024) *(u32x4*)(os + b) = *(const u32x4*)(stage + b);
+    if (threadIdx.x == 0) sink[blockIdx.x] = *(const unsigned*)smem ^ *(const unsigned*)(smem + kv_span);
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+}  // namespace
+}  // namespace sdattn
+
+using namespace sdattn;
+
+extern "C" int sdattn_probe_mix(int mode, int blocks, int it_m, int it_v, float* out,
+                                unsigned long long* clk, void* stream) {
+    if (!out || mode < 0 || mode > 7 || blocks < 1 || blocks > 65536 || it_m < 0 || it_v < 0 ||
+        it_m > (1 << 20) || it_v > (1 << 20))
+        return (int)hipErrorInvalidValue;
+    hipLaunchKernelGGL(mix_kernel, dim3(blocks), dim3(512), 0, (hipStream_t)stream, out, mode, it_m, it_v, clk);
+    return (int)hipGetLastError();
+}
+
+extern "C" int sdattn_probe_copy(const void* src, void* dst, long long bytes, int blocks, void* stream) {
+    if (!src || !dst || bytes < 16 || bytes % 16 || blocks < 1 || blocks > (1 << 20) || !aligned16(src) ||
+        !aligned16(dst))
+        return (int)hipErrorInvalidValue;
+    const char* s = (const char*)src;
+    const char* d = (const char*)dst;
+    if (s < d + bytes && d < s + bytes) return (int)hipErrorInvalidValue;
+    hipLaunchKernelGGL(copy_kernel, dim3(blocks), dim3(256), 0, (hipStream_t)stream, (const u32x4*)src,
+                       (u32x4*)dst, bytes / 16);
+    return (int)hipGetLastError();
+}
+
+extern "C" int sdattn_probe_read(const void* src, long long bytes, unsigned* sink, int blocks, void* stream) {
+    if (!src || !sink || bytes < 16 || bytes % 16 || blocks < 1 || blocks > (1 << 20) || !aligned16(src))
+        return (int)hipErrorInvalidValue;
+    hipLaunchKernelGGL(read_kernel, dim3(blocks), dim3(256), 0, (hipStream_t)stream, (const u32x4*)src,
+                       bytes / 16, sink);
+    return (int)hipGetLastError();
+}
+
+extern "C" int sdattn_probe_strip_copy(const void* q, const void* k, const void* v, void* o, unsigned* sink,
+                                       int B, int H, int Lq, int Lk, int D, void* stream) {
+    if (!q || !k || !v || !o || !sink || B < 1 || H < 1 || Lq < 1 || Lk < 1 || Lk > 128 || D < 8 || D > 160 ||
+        D % 8 || !aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o))
+        return (int)hipErrorInvalidValue;
+    const int nqb = (Lq + 255) / 256;
+    const long long nblk = (long long)B * H * nqb;
+    if (nblk > (1 << 24)) return (int)hipErrorInvalidValue;
+    const int kv_span = (Lk * D * 2 + 1023) / 1024 * 1024;
+    const int lds = 2 * kv_span + 8 * 32 * D * 2;   // <= 2 * 40 KiB + 80 KiB
+    static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(strip_copy_kernel),
+                                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (attr != hipSuccess) return (int)attr;
+    hipLaunchKernelGGL(strip_copy_kernel, dim3((unsigned)nblk), dim3(512), lds, (hipStream_t)stream,
+                       (const char*)q, (const char*)k, (const char*)v, (char*)o, sink, Lq, Lk, D, nqb, kv_span);
+    return (int)hipGetLastError();
+}

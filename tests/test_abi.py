@@ -334,3 +334,24 @@ def test_winograd_checks_and_table2_factors(lib):
     assert cv(x=ctypes.c_void_p(0x10000008)) == MISALIGNED
     assert cv(y=ctypes.c_void_p(0x10000000 + 256)) == INVALID      # y overlaps x
     assert cv(ws=ctypes.c_void_p(0x60000000 + 512)) == INVALID     # workspace overlaps u
+
+
+# ------------------------------------------------ the measurement kernels
+
+def test_probe_library_exports_every_declared_symbol():
+    from paper_2304_11267_amd import probes
+    if not os.path.exists(probes.library_path()):
+        pytest.skip("libsdattn_probes.so not built")
+    text = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "sdattn_probes.h")).read(), flags=re.S)
+    declared = sorted(set(re.findall(r"\b(sdattn_probe_\w+)\s*\(", text)))
+    assert declared == sorted(probes.EXPORTS)
+    plib = probes.load_library()
+    for name in declared:
+        assert hasattr(plib, name), name
+    # out-of-range arguments are refused before any launch (hipErrorInvalidValue = 1)
+    assert plib.sdattn_probe_mix(9, 1, 1, 1, QA, None, None) == 1
+    assert plib.sdattn_probe_copy(QA, KA, 15, 1, None) == 1
+    assert plib.sdattn_probe_copy(QA, ctypes.c_void_p(0x10000010), 4096, 1, None) == 1   # overlap
+    assert plib.sdattn_probe_read(QA, 0, KA, 1, None) == 1
+    assert plib.sdattn_probe_strip_copy(QA, KA, VA, OA, LA, 2, 8, 4096, 77, 12, None) == 1
+    assert plib.sdattn_probe_strip_copy(QA, KA, VA, OA, LA, 2, 8, 4096, 129, 40, None) == 1

@@ -44,7 +44,8 @@ typedef enum {
     SDATTN_ERR_INVALID_ARG = 1,  /* NULL pointer, size < 1, non-finite scale, overlap, bad dtype */
     SDATTN_ERR_UNSUPPORTED = 2,  /* D not a multiple of 8, D > 256, or a grid too large */
     SDATTN_ERR_MISALIGNED = 3,   /* a pointer is not aligned as documented */
-    SDATTN_ERR_HIP = 4           /* a HIP runtime call failed; see sdattn_last_hip_error() */
+    SDATTN_ERR_HIP = 4,          /* a HIP runtime call failed; see sdattn_last_hip_error() */
+    SDATTN_ERR_SCRATCH = 5       /* more workspace than SDATTN_STATIC_SCRATCH_BYTES */
 } sdattn_status;
 
 typedef enum {
@@ -192,6 +193,28 @@ int sdattn_attention_block(const void *x, const void *ctx, const void *wq, const
                            const void *wv, const void *wo, const void *bo, void *out,
                            void *workspace, long long workspace_bytes, int B, int Lq, int Lk,
                            int C, int Cc, int H, float scale, sdattn_dtype dtype, void *stream);
+
+/*
+ * sdattn_attention_block without a caller workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, serving loops,
+ * harnesses that forbid hipMalloc): Q, K, V and O go through a static scratch
+ * of SDATTN_STATIC_SCRATCH_BYTES that the library holds on each GPU it runs
+ * on until the process ends.  The call allocates nothing; its first call on a
+ * device looks up that device's scratch address (no launch).
+ *
+ * Arguments as for sdattn_attention_block, minus the workspace; the scratch
+ * belongs to the current device, so `stream` must belong to it too.
+ * Returns SDATTN_ERR_SCRATCH, before any HIP call, when
+ * sdattn_attention_block_workspace(B, Lq, Lk, C) exceeds the scratch (every
+ * SD1.4 block at B = 2 fits: 21 MB at the 64x64 level).  Every call on one
+ * GPU shares that GPU's scratch: calls that may overlap on one GPU (other
+ * streams, other host threads) race and must be ordered by the caller.
+ */
+#define SDATTN_STATIC_SCRATCH_BYTES (32LL << 20)
+int sdattn_attention_block_static(const void *x, const void *ctx, const void *wq, const void *wk,
+                                  const void *wv, const void *wo, const void *bo, void *out, int B,
+                                  int Lq, int Lk, int C, int Cc, int H, float scale,
+                                  sdattn_dtype dtype, void *stream);
 
 /*
  * The context side of a cross-attention block: K = ctx wk^T and V = ctx wv^T,

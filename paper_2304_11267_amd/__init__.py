@@ -8,11 +8,11 @@ falling back to anything else.
 """
 from .binding import (  # noqa: F401
     SdattnError, forward, forward_ex, softmax_rows, logits, softmax_pv, linear,
-    attention_block_workspace, attention_block, project_kv, attention_block_kv, group_norm, geglu,
+    attention_block_workspace, attention_block, attention_block_static, project_kv, attention_block_kv, group_norm, geglu,
     winograd_weights, conv3x3_workspace, conv3x3,
     library_path,
     load_library,
     LAYOUT_ROWS, LAYOUT_HEADS,
-    STATUS_OK, STATUS_INVALID_ARG, STATUS_UNSUPPORTED, STATUS_MISALIGNED, STATUS_HIP,
+    STATUS_OK, STATUS_INVALID_ARG, STATUS_UNSUPPORTED, STATUS_MISALIGNED, STATUS_HIP, STATUS_SCRATCH,
     DTYPE_F16, DTYPE_BF16, DTYPE_F32,
 )

@@ -20,6 +20,7 @@ STATUS_INVALID_ARG = 1
 STATUS_UNSUPPORTED = 2
 STATUS_MISALIGNED = 3
 STATUS_HIP = 4
+STATUS_SCRATCH = 5
 
 DTYPE_F16 = 0
 DTYPE_BF16 = 1
@@ -28,7 +29,8 @@ DTYPE_F32 = 2
 # every symbol include/sdattn.h declares
 EXPORTS = ("sdattn_forward", "sdattn_forward_ex", "sdattn_softmax_rows", "sdattn_logits",
            "sdattn_softmax_pv", "sdattn_linear", "sdattn_attention_block_workspace",
-           "sdattn_attention_block", "sdattn_project_kv", "sdattn_attention_block_kv",
+           "sdattn_attention_block", "sdattn_attention_block_static", "sdattn_project_kv",
+           "sdattn_attention_block_kv",
            "sdattn_group_norm", "sdattn_geglu", "sdattn_winograd_weights_elems",
            "sdattn_winograd_weights", "sdattn_conv3x3_workspace", "sdattn_conv3x3",
            "sdattn_status_str", "sdattn_last_hip_error", "sdattn_version")
@@ -78,6 +80,9 @@ def load_library():
     lib.sdattn_attention_block.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i64, i32, i32, i32,
                                            i32, i32, i32, f32, i32, vp]
     lib.sdattn_attention_block.restype = i32
+    lib.sdattn_attention_block_static.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i32, i32, i32, i32,
+                                                  i32, i32, f32, i32, vp]
+    lib.sdattn_attention_block_static.restype = i32
     lib.sdattn_project_kv.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp]
     lib.sdattn_project_kv.restype = i32
     lib.sdattn_attention_block_kv.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i64, i32, i32, i32,
@@ -273,6 +278,24 @@ def attention_block(x, ctx, wq, wk, wv, wo, bo, out, workspace, heads, scale, st
         _dev(workspace, "workspace"), workspace.numel() * workspace.element_size(),
         B, Lq, Lk, C, Cc, heads, ctypes.c_float(scale), _dtype_code(x), _stream(stream))
     _check("sdattn_attention_block", status)
+    return out
+
+
+def attention_block_static(x, ctx, wq, wk, wv, wo, bo, out, heads, scale, stream=None):
+    """attention_block through the library's static scratch (no workspace argument)."""
+    B, Lq, C = x.shape
+    Lk, Cc = ctx.shape[1], ctx.shape[2]
+    _expect(ctx, (B, Lk, Cc), x, "ctx")
+    for t, shape, name in ((wq, (C, C), "wq"), (wk, (C, Cc), "wk"), (wv, (C, Cc), "wv"),
+                           (wo, (C, C), "wo"), (out, (B, Lq, C), "out")):
+        _expect(t, shape, x, name)
+    if bo is not None:
+        _expect(bo, (C,), x, "bo")
+    status = load_library().sdattn_attention_block_static(
+        _dev(x, "x"), _dev(ctx, "ctx"), _dev(wq, "wq"), _dev(wk, "wk"), _dev(wv, "wv"),
+        _dev(wo, "wo"), _dev(bo, "bo") if bo is not None else None, _dev(out, "out"),
+        B, Lq, Lk, C, Cc, heads, ctypes.c_float(scale), _dtype_code(x), _stream(stream))
+    _check("sdattn_attention_block_static", status)
     return out
 
 

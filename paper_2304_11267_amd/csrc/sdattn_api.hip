@@ -5,9 +5,17 @@
 #include <stdint.h>
 
 #include <climits>
+#include <mutex>
 
 #include "launch.h"
 #include "sdattn.h"
+
+// The static scratch of sdattn_attention_block_static: Q, K, V and O of one
+// block between its launches, for callers that cannot allocate.  Each GPU the
+// library runs on holds its own copy until the process ends.  In host code
+// `scratch` names a host-side stand-in, never the device memory: its device
+// address comes from hipGetSymbolAddress, once per device (scratch_address).
+static __device__ __align__(256) char scratch[SDATTN_STATIC_SCRATCH_BYTES];
 
 namespace {
 
@@ -30,6 +38,34 @@ long long checked_mul(std::initializer_list<long long> fs) {
         r *= f;
     }
     return r < (1LL << 62) ? r : -1;
+}
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices] = {};
+
+// The current device's address of `scratch`, looked up on the first call on
+// that device (with it current) and kept: no allocation, no launch.
+int scratch_address(void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) {
+        g_last_hip_error = (int)e;
+        return SDATTN_ERR_HIP;
+    }
+    if (dev < 0 || dev >= kMaxScratchDevices) return SDATTN_ERR_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p) {
+            g_last_hip_error = (int)(e != hipSuccess ? e : hipErrorInvalidSymbol);
+            return SDATTN_ERR_HIP;
+        }
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return SDATTN_OK;
 }
 
 int finish(hipError_t e) {
@@ -276,6 +312,24 @@ int sdattn_attention_block(const void* x, const void* ctx, const void* wq, const
     return finish(sdattn::launch_linear(po));
 }
 
+int sdattn_attention_block_static(const void* x, const void* ctx, const void* wq, const void* wk,
+                                  const void* wv, const void* wo, const void* bo, void* out, int B,
+                                  int Lq, int Lk, int C, int Cc, int H, float scale,
+                                  sdattn_dtype dtype, void* stream) {
+    // what needs no device address first: a refused size makes no HIP call
+    if (!x || !ctx || !wq || !wk || !wv || !wo || !out) return SDATTN_ERR_INVALID_ARG;
+    if (B < 1 || Lq < 1 || Lk < 1 || C < 1 || Cc < 1 || H < 1) return SDATTN_ERR_INVALID_ARG;
+    if (C % H != 0) return SDATTN_ERR_INVALID_ARG;
+    const long long need = sdattn_attention_block_workspace(B, Lq, Lk, C);
+    if (need < 0) return SDATTN_ERR_UNSUPPORTED;
+    if (need > SDATTN_STATIC_SCRATCH_BYTES) return SDATTN_ERR_SCRATCH;
+    void* ws = nullptr;
+    const int st = scratch_address(&ws);
+    if (st != SDATTN_OK) return st;
+    return sdattn_attention_block(x, ctx, wq, wk, wv, wo, bo, out, ws, SDATTN_STATIC_SCRATCH_BYTES, B, Lq,
+                                  Lk, C, Cc, H, scale, dtype, stream);
+}
+
 int sdattn_project_kv(const void* ctx, const void* wk, const void* wv, void* k, void* v, int B,
                       int Lk, int Cc, int C, int H, sdattn_dtype dtype, void* stream) {
     if (!ctx || !wk || !wv || !k || !v) return SDATTN_ERR_INVALID_ARG;
@@ -439,6 +493,7 @@ const char* sdattn_status_str(int status) {
         case SDATTN_ERR_UNSUPPORTED: return "unsupported size or type";
         case SDATTN_ERR_MISALIGNED: return "misaligned pointer";
         case SDATTN_ERR_HIP: return "HIP runtime error";
+        case SDATTN_ERR_SCRATCH: return "needs more than the static scratch holds";
         default: return "unknown status";
     }
 }

@@ -229,6 +229,31 @@ def test_attention_block_checks(lib):
     assert blk(lib, x=ctypes.c_void_p(0x60000000 + 1024)) == INVALID     # x inside the workspace
 
 
+def test_attention_block_static_refuses_before_any_hip_call(lib):
+    # the sizes and pointers it can check without the scratch's device address
+    def bst(**kw):
+        a = dict(x=QA, ctx=KA, wq=ctypes.c_void_p(0x70000000), wk=ctypes.c_void_p(0x71000000),
+                 wv=ctypes.c_void_p(0x72000000), wo=ctypes.c_void_p(0x73000000),
+                 bo=ctypes.c_void_p(0x74000000), out=OA, B=2, Lq=64, Lk=77, C=320, Cc=768, H=8,
+                 scale=0.158, dtype=F16)
+        a.update(kw)
+        return lib.sdattn_attention_block_static(a["x"], a["ctx"], a["wq"], a["wk"], a["wv"], a["wo"],
+                                                 a["bo"], a["out"], a["B"], a["Lq"], a["Lk"], a["C"],
+                                                 a["Cc"], a["H"], ctypes.c_float(a["scale"]), a["dtype"],
+                                                 None)
+    SCRATCH = 5
+    for field in ("x", "ctx", "wq", "wk", "wv", "wo", "out"):
+        assert bst(**{field: None}) == INVALID
+    assert bst(B=0) == INVALID
+    assert bst(C=321) == INVALID                        # heads do not divide C
+    # 32 MiB of scratch: the 64x64-level self block at B = 2 needs 21 MB, at B = 4 42 MB
+    assert lib.sdattn_attention_block_workspace(2, 4096, 4096, 320) <= 32 << 20
+    assert lib.sdattn_attention_block_workspace(4, 4096, 4096, 320) > 32 << 20
+    assert bst(B=4, Lq=4096, Lk=4096, C=320, Cc=320) == SCRATCH
+    assert lib.sdattn_status_str(SCRATCH) == b"needs more than the static scratch holds"
+    assert lib.sdattn_last_hip_error() == 0
+
+
 def test_project_kv_checks(lib):
     W1, W2 = ctypes.c_void_p(0x71000000), ctypes.c_void_p(0x72000000)
 

@@ -526,29 +526,35 @@ def cross_floor(torch, wl, dev, stream, case, nsets=40):
         k = torch.randn(case.B, case.H, case.Lk, case.D, device=dev, generator=g).half()
         v = torch.randn(case.B, case.H, case.Lk, case.D, device=dev, generator=g).half()
         sets.append((q, k, v, torch.empty_like(q)))
-    sink = torch.empty(case.B * case.H * ((case.Lq + 255) // 256), dtype=torch.int32, device=dev)
+    sink = torch.empty(case.B * case.H * ((case.Lq + 63) // 64), dtype=torch.int32, device=dev)
     launches = 5 * nsets
 
-    def batch(rot):
+    def batch(rot, waves):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda._sleep(20_000_000)
         e0.record(stream)
         for i in range(launches):
             s = sets[i % nsets] if rot else sets[0]
-            probes.strip_copy(*s, sink, stream)
+            probes.strip_copy(*s, sink, waves, stream)
         e1.record(stream)
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / launches
 
-    for s in sets:
-        probes.strip_copy(*s, sink, stream)
-    torch.cuda.synchronize()
-    cold = min(batch(True) for _ in range(3))
-    warm = min(batch(False) for _ in range(3))
-    return {"cold_us": round(cold * 1e3, 3), "cold_gbs": round(case.bytes / (cold * 1e-3) / 1e9, 1),
-            "warm_us": round(warm * 1e3, 3), "warm_gbs": round(case.bytes / (warm * 1e-3) / 1e9, 1),
-            "what": "plain copy of Q to O plus reads of K, V with the cross kernel's grid, "
-                    f"{nsets} rotated input sets (cold) or one (warm), back-to-back launches"}
+    res = {}
+    for waves in (8, 4, 2):
+        for s in sets:
+            probes.strip_copy(*s, sink, waves, stream)
+        torch.cuda.synchronize()
+        cold = min(batch(True, waves) for _ in range(3))
+        warm = min(batch(False, waves) for _ in range(3))
+        res[f"waves{waves}"] = {"cold_us": round(cold * 1e3, 3),
+                                "cold_gbs": round(case.bytes / (cold * 1e-3) / 1e9, 1),
+                                "warm_us": round(warm * 1e3, 3),
+                                "warm_gbs": round(case.bytes / (warm * 1e-3) / 1e9, 1)}
+    res["what"] = ("plain copy of Q to O plus reads of K, V in workgroups of 8, 4 or 2 strips of 32 rows "
+                   f"(the cross kernel launches 8), {nsets} rotated input sets (cold) or one (warm), "
+                   "back-to-back launches")
+    return res
 
 
 def bench_sweep(torch, sd, wl, dev, stream, steps=20, launches=20):

@@ -48,14 +48,14 @@ int sdattn_probe_read(const void* src, long long bytes, unsigned* sink, int bloc
 
 /* The cross-attention kernel's data movement without its arithmetic: for
  * Q [B,H,Lq,D] and K, V [B,H,Lk,D] (16-bit elements, D % 8 == 0, D <= 160,
- * Lk <= 128), workgroups of eight waves each take 256 query rows of one
- * (b, h) (one 32-row strip per wave, the same XCD remap of the workgroup
- * index), copy all of that head's K and V and their Q rows into LDS with
- * 16-byte direct copies, and after one barrier store the Q rows to
+ * Lk <= 128), workgroups of `waves` waves (2, 4 or 8) each take 32 * waves
+ * query rows of one (b, h) (one 32-row strip per wave, the same XCD remap of
+ * the workgroup index), copy all of that head's K and V and their Q rows into
+ * LDS with 16-byte direct copies, and after one barrier store the Q rows to
  * O [B,H,Lq,D] unchanged; sink receives one word per workgroup
- * (B * H * ceil(Lq / 256) words). */
+ * (B * H * ceil(Lq / (32 * waves)) words). */
 int sdattn_probe_strip_copy(const void* q, const void* k, const void* v, void* o, unsigned* sink,
-                            int B, int H, int Lq, int Lk, int D, void* stream);
+                            int B, int H, int Lq, int Lk, int D, int waves, void* stream);
 
 #ifdef __cplusplus
 }

@@ -20,8 +20,8 @@
 // last sub-tile mask p past Lk.  The P V product skips a final 16-key step
 // that lies wholly past Lk.  A negative scale negates K once in LDS.
 //
-// A workgroup holds W waves (one 32-row strip each) and loads K and V once
-// for all of them: W = 8 when the grid still fills every CU, else 4.
+// A workgroup holds W = 4 waves (one 32-row strip each) and loads K and V
+// once for all of them.
 //
 // Operand layouts are those of the long-sequence kernel: S^T = K Q^T and
 // O^T = V^T P^T on 32x32x16 MFMAs with one query per lane, V^T produced by
@@ -305,14 +305,11 @@ hipError_t launch_short_dnw(const AttnArgs& a) {
     return hipGetLastError();
 }
 
-// Eight waves per workgroup once there are at least eight 32-row strips per CU
-// (256 CUs) and the LDS allows it; four otherwise.
+// Four waves per workgroup: at the 64x64 level (2048 strips) this makes two
+// workgroups per CU with their own barriers, which measured faster with cold
+// inputs than one workgroup of eight (5.24 vs 5.47 us; two waves: 5.77).
 template <int ET, int D, int NS>
 hipError_t launch_short_dn(const AttnArgs& a) {
-    const long long strips = (long long)a.B * a.H * ((a.Lq + 31) / 32);
-    if constexpr (ShortGeom<D, NS, 8>::kFits) {
-        if (strips >= 8 * 256) return launch_short_dnw<ET, D, NS, 8>(a);
-    }
     return launch_short_dnw<ET, D, NS, 4>(a);
 }
 

@@ -100,16 +100,15 @@ __global__ __launch_bounds__(256) void read_kernel(const u32x4* __restrict__ src
     sink[(size_t)blockIdx.x * blockDim.x + threadIdx.x] = x[0] ^ x[1] ^ x[2] ^ x[3];
 }
 
-// Eight waves per workgroup, 256 query rows of one head: the data movement of
-// the short-sequence attention kernel's large-grid launch without its
-// arithmetic.  K and V (all Lk rows) and each wave's 32 query rows go
+// W waves per workgroup (one 32-row strip each) of one head: the data
+// movement of the short-sequence attention kernel without its arithmetic.  K and V (all Lk rows) and each wave's 32 query rows go
 // global -> LDS with 16-byte direct copies, all issued before any wait; after
 // the workgroup's barrier each wave stores its rows back out as O with
 // 16-byte lanes, as the kernel's epilogue does.
 __global__ __launch_bounds__(512) void strip_copy_kernel(const char* __restrict__ Q, const char* __restrict__ K,
                                                          const char* __restrict__ V, char* __restrict__ O,
                                                          unsigned* __restrict__ sink, int Lq, int Lk, int D,
-                                                         int nqb, int kv_span) {
+                                                         int nqb, int kv_span, int W) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     const int tile = xcd_remap(blockIdx.x, gridDim.x);
     const int bh = tile / nqb;
@@ -119,7 +118,7 @@ __global__ __launch_bounds__(512) void strip_copy_kernel(const char* __restrict_
     const char* kh = K + (size_t)bh * kv_bytes;
     const char* vh = V + (size_t)bh * kv_bytes;
     const int nkv = kv_span / 1024;
-    for (int c = wave; c < 2 * nkv; c += 8) {
+    for (int c = wave; c < 2 * nkv; c += W) {
         const bool isv = c >= nkv;
         const int cc = isv ? c - nkv : c;
         const int byte = cc * 1024 + lane * 16;
@@ -128,7 +127,7 @@ __global__ __launch_bounds__(512) void strip_copy_kernel(const char* __restrict_
                                              (lds_void_t*)(smem + (isv ? kv_span : 0) + cc * 1024), 16, 0, 0);
     }
     const int strip = 32 * D * 2;
-    const int q0 = qb * 256 + wave * 32;
+    const int q0 = qb * 32 * W + wave * 32;
     const int bytes = max(0, min(32, Lq - q0)) * D * 2;
     char* stage = smem + 2 * kv_span + wave * strip;
     const char* qs = Q + ((size_t)bh * Lq + max(q0, 0)) * D * 2;
@@ -180,19 +179,21 @@ extern "C" int sdattn_probe_read(const void* src, long long bytes, unsigned* sin
 }
 
 extern "C" int sdattn_probe_strip_copy(const void* q, const void* k, const void* v, void* o, unsigned* sink,
-                                       int B, int H, int Lq, int Lk, int D, void* stream) {
+                                       int B, int H, int Lq, int Lk, int D, int waves, void* stream) {
     if (!q || !k || !v || !o || !sink || B < 1 || H < 1 || Lq < 1 || Lk < 1 || Lk > 128 || D < 8 || D > 160 ||
-        D % 8 || !aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o))
+        D % 8 || (waves != 2 && waves != 4 && waves != 8) || !aligned16(q) || !aligned16(k) || !aligned16(v) ||
+        !aligned16(o))
         return (int)hipErrorInvalidValue;
-    const int nqb = (Lq + 255) / 256;
+    const int nqb = (Lq + 32 * waves - 1) / (32 * waves);
     const long long nblk = (long long)B * H * nqb;
     if (nblk > (1 << 24)) return (int)hipErrorInvalidValue;
     const int kv_span = (Lk * D * 2 + 1023) / 1024 * 1024;
-    const int lds = 2 * kv_span + 8 * 32 * D * 2;   // <= 2 * 40 KiB + 80 KiB
+    const int lds = 2 * kv_span + waves * 32 * D * 2;   // <= 2 * 40 KiB + 80 KiB
     static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(strip_copy_kernel),
                                                        hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     if (attr != hipSuccess) return (int)attr;
-    hipLaunchKernelGGL(strip_copy_kernel, dim3((unsigned)nblk), dim3(512), lds, (hipStream_t)stream,
-                       (const char*)q, (const char*)k, (const char*)v, (char*)o, sink, Lq, Lk, D, nqb, kv_span);
+    hipLaunchKernelGGL(strip_copy_kernel, dim3((unsigned)nblk), dim3(64 * waves), lds, (hipStream_t)stream,
+                       (const char*)q, (const char*)k, (const char*)v, (char*)o, sink, Lq, Lk, D, nqb, kv_span,
+                       waves);
     return (int)hipGetLastError();
 }

@@ -38,7 +38,7 @@ def load_library():
     lib.sdattn_probe_mix.argtypes = [i32, i32, i32, i32, vp, vp, vp]
     lib.sdattn_probe_copy.argtypes = [vp, vp, i64, i32, vp]
     lib.sdattn_probe_read.argtypes = [vp, i64, vp, i32, vp]
-    lib.sdattn_probe_strip_copy.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, vp]
+    lib.sdattn_probe_strip_copy.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp]
     for name in EXPORTS:
         getattr(lib, name).restype = i32
     _lib = lib
@@ -72,8 +72,8 @@ def read(src, nbytes, sink, blocks, stream=None):
         ctypes.c_void_p(src.data_ptr()), nbytes, ctypes.c_void_p(sink.data_ptr()), blocks, _stream(stream)))
 
 
-def strip_copy(q, k, v, o, sink, stream=None):
+def strip_copy(q, k, v, o, sink, waves=8, stream=None):
     B, H, Lq, D = q.shape
     Lk = k.shape[2]
     _check("sdattn_probe_strip_copy", load_library().sdattn_probe_strip_copy(
-        *(ctypes.c_void_p(t.data_ptr()) for t in (q, k, v, o, sink)), B, H, Lq, Lk, D, _stream(stream)))
+        *(ctypes.c_void_p(t.data_ptr()) for t in (q, k, v, o, sink)), B, H, Lq, Lk, D, waves, _stream(stream)))

@@ -378,5 +378,6 @@ def test_probe_library_exports_every_declared_symbol():
     assert plib.sdattn_probe_copy(QA, KA, 15, 1, None) == 1
     assert plib.sdattn_probe_copy(QA, ctypes.c_void_p(0x10000010), 4096, 1, None) == 1   # overlap
     assert plib.sdattn_probe_read(QA, 0, KA, 1, None) == 1
-    assert plib.sdattn_probe_strip_copy(QA, KA, VA, OA, LA, 2, 8, 4096, 77, 12, None) == 1
-    assert plib.sdattn_probe_strip_copy(QA, KA, VA, OA, LA, 2, 8, 4096, 129, 40, None) == 1
+    assert plib.sdattn_probe_strip_copy(QA, KA, VA, OA, LA, 2, 8, 4096, 77, 12, 8, None) == 1
+    assert plib.sdattn_probe_strip_copy(QA, KA, VA, OA, LA, 2, 8, 4096, 129, 40, 8, None) == 1
+    assert plib.sdattn_probe_strip_copy(QA, KA, VA, OA, LA, 2, 8, 4096, 77, 40, 3, None) == 1

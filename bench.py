@@ -57,6 +57,9 @@ def parse():
                     help="also run a plain 256 MiB device copy (scales the HBM traffic counters)")
     ap.add_argument("--no-sweep", action="store_true", help="skip the 20-step UNet sweep")
     ap.add_argument("--no-probes", action="store_true", help="skip the measured-peak probes")
+    ap.add_argument("--lk-scaling", action="store_true",
+                    help="also time the 64x64 self-attention kernel at Lk = 256 .. 4096 (fixed cost and "
+                         "cost per 128-key tile by a least-squares line)")
     return ap.parse_args()
 
 
@@ -187,6 +190,9 @@ def main():
 
     if not args.no_sweep:
         out["sweep"] = bench_sweep(torch, sd, wl, dev, stream)
+
+    if args.lk_scaling:
+        out["lk_scaling"] = lk_scaling(torch, sd, wl, dev, stream, self_case)
 
     if args.copy_calibration:
         out["copy_calibration"] = copy_calibration(torch, dev, stream)
@@ -612,6 +618,29 @@ def bench_sweep(torch, sd, wl, dev, stream, steps=20, launches=20):
             "levels": levels,
             "inputs": "per call N(0,1) fp16 from torch's GPU generator seeded with the call's seed "
                       "(S0 + 1000(t+1) + 10b, +1 for cross)"}
+
+
+def lk_scaling(torch, sd, wl, dev, stream, case, lks=(256, 512, 1024, 2048, 3072, 4096)):
+    """The 64x64-level self-attention kernel (B2 H8 Lq 4096 D40, the same
+    256-row workgroups) at several key counts: the least-squares line through
+    the average launch times splits the kernel into a fixed part (launch,
+    Q load, first tile, the key halves' merge, epilogue) and a cost per
+    128-key tile of each key half (two tiles per 256 keys)."""
+    pts = []
+    for lk in lks:
+        q, k, v = wl.make_qkv(case.B, case.H, case.Lq, lk, case.D, case.seed)
+        qd, kd, vd = (torch.from_numpy(t).to(dev) for t in (q, k, v))
+        ms = back_to_back_ms(torch, sd, stream, [(qd, kd, vd, torch.empty_like(qd))], case.scale,
+                             launches=50)
+        pts.append((lk, ms * 1e3))
+    xs = np.array([p[0] / 256.0 for p in pts])   # 128-key tiles per key half
+    ys = np.array([p[1] for p in pts])
+    slope, icept = np.polyfit(xs, ys, 1)
+    return {"points_us": {str(lk): round(us, 3) for lk, us in pts},
+            "fixed_us": round(float(icept), 3), "per_tile_us": round(float(slope), 4),
+            "tiles_at_4096": 16,
+            "what": "B2 H8 Lq4096 D40 self-attention at Lk = 256..4096, back-to-back launches; "
+                    "line through (tiles per key half, us)"}
 
 
 def copy_calibration(torch, dev, stream, nbytes=256 << 20, reps=3):

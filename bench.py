@@ -500,6 +500,14 @@ def measured_peaks(torch, dev, stream):
         res[f"overlap_mfma_{name}"] = round((hi - both) / (hi - lo), 3) if hi > lo else None
         res[f"mfma_{name}_us"] = {"mfma_alone": round(half_m * 1e3, 1), f"{name}_alone": round(alone_v * 1e3, 1),
                                   "together": round(both * 1e3, 1)}
+    # the D = 40 tile's instruction mix without data movement: ns per 32x32 pair per SIMD
+    ti = 4000
+    pairs_per_simd = 2 * ti * 2           # two waves per SIMD, two pairs per iteration
+    for key, exps, noise in (("tile_mix_ns_per_pair", True, False), ("tile_mix_no_exp_ns_per_pair", False, False),
+                             ("tile_mix_noise_ns_per_pair", True, True),
+                             ("tile_mix_noise_no_exp_ns_per_pair", False, True)):
+        t = _events_ms(torch, stream, lambda: probes.tile(256, ti, exps, out, noise, stream))
+        res[key] = round(t * 1e6 / pairs_per_simd, 2)
     # HBM streaming (buffers far beyond the 256 MB Infinity Cache)
     n = 1 << 30
     src = torch.empty(n, dtype=torch.uint8, device=dev)

@@ -36,6 +36,18 @@ extern "C" {
 int sdattn_probe_mix(int mode, int blocks, int it_m, int it_v, float* out,
                      unsigned long long* clk, void* stream);
 
+/* The D = 40 self-attention tile's instruction mix without its data
+ * movement: `blocks` workgroups of eight waves (two per SIMD), each wave
+ * `iters` iterations of two 32-query x 32-key pairs that share every operand
+ * read -- K rows from a static LDS tile into 2 x 3 chained 32x32x16 MFMAs,
+ * per pair 16 v_fma_f32, 16 v_exp_f32 and 8 conversions, V^T by
+ * transposing LDS reads into 2 x 4 MFMAs.  mode bit 0: with the
+ * exponentials; bit 1: operands of random sign and mantissa (bits that toggle
+ * like real activations) instead of near-constant ones.
+ * out: blocks * 512 floats.  Limits: 1 <= blocks <= 65536, 1 <= iters <= 1 << 20,
+ * 0 <= mode <= 3. */
+int sdattn_probe_tile(int blocks, int iters, int mode, float* out, void* stream);
+
 /* dst[0 .. bytes) = src[0 .. bytes) with 16-byte loads and stores, grid-stride
  * over `blocks` workgroups of 256 threads.  bytes % 16 == 0, pointers 16-byte
  * aligned, the two ranges disjoint. */

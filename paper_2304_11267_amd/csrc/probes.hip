@@ -54,6 +54,122 @@ __device__ __forceinline__ float valu_stream(int iters) {
     return s;
 }
 
+// The self-attention tile's instruction mix without its data movement: per
+// iteration two 32-query x 32-key pairs sharing every operand read, as the
+// D = 40 kernel runs them -- K rows from LDS (three 16-byte reads) into 2 x 3
+// chained 32x32x16 MFMAs, then per pair 16 FMAs (c s - m), 16 exponentials
+// and 8 conversions, then V^T by transposing LDS reads into 2 x 4 MFMAs.
+// The LDS tile is written once and only read; exps = 0 leaves out the
+// exponentials.  Returns nothing but a checksum per lane.
+__device__ __forceinline__ uint32_t pack_h2(float x, float y) {
+    typedef float f2 __attribute__((ext_vector_type(2)));
+    typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+    const f2 v = {x, y};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, h2));
+}
+
+__device__ __forceinline__ f32x16 mm32(u32x4 a, u32x4 b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c,
+                                                  0, 0, 0);
+}
+
+template <bool EXPS>
+__device__ __forceinline__ void tile_softmax(const f32x16& st, float c, float m, u32x4 (&p)[2]) {
+    float e[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) e[r] = fmaf(st[r], c, -m);
+    if constexpr (EXPS) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) e[r] = __builtin_amdgcn_exp2f(e[r]);
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int w = 0; w < 4; ++w) p[u][w] = pack_h2(e[8 * u + 2 * w], e[8 * u + 2 * w + 1]);
+}
+
+// fp16 pairs of random sign and mantissa with magnitudes in [1/4, 2): operand
+// bits that toggle like real activations (the matrix core's power, and so the
+// clock it sustains, depends on them)
+__device__ __forceinline__ uint32_t noise_h2(uint32_t i) {
+    const uint32_t h = i * 2654435761u ^ (i >> 7) * 40503u;
+    const uint32_t lo = (h & 0x83ffu) | (0x3400u + ((h >> 10) & 0x0c00u));
+    const uint32_t g = h * 2246822519u;
+    const uint32_t hi = (g & 0x83ffu) | (0x3400u + ((g >> 10) & 0x0c00u));
+    return lo | (hi << 16);
+}
+
+template <bool EXPS, bool NOISE>
+__device__ float tile_mix(int iters) {
+    constexpr int D = 40;
+    __shared__ __attribute__((aligned(16))) char lds[32 * 1024];
+    for (int i = threadIdx.x; i < 32 * 1024 / 16; i += 512)
+        *(u32x4*)(lds + 16 * i) = NOISE ? u32x4{noise_h2(4 * i), noise_h2(4 * i + 1), noise_h2(4 * i + 2), noise_h2(4 * i + 3)}
+                                        : u32x4{0x2c002c00u, 0x3c00u, (uint32_t)i & 0x3ffu, 0x2c00u};
+    __syncthreads();
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, l32 = lane & 31, half = lane >> 5;
+    const char* base = lds + (wave & 3) * 8192;   // 64 keys of K (5 KiB), then V
+    const int k_off = (l32 * D + 8 * half) * 2;
+    const int g = lane >> 4, i16 = lane & 15;
+    const int v_off = 64 * D * 2 + ((4 * (g >> 1) + (i16 >> 2)) * D + 16 * (g & 1) + 4 * (i16 & 3)) * 2;
+    u32x4 q0[3], q1[3];
+#pragma unroll
+    for (int s = 0; s < 3; ++s) {
+        if constexpr (NOISE) {
+            const uint32_t b = 4096u * (uint32_t)(threadIdx.x * 3 + s);
+            q0[s] = u32x4{noise_h2(b), noise_h2(b + 1), noise_h2(b + 2), noise_h2(b + 3)};
+        } else {
+            q0[s] = u32x4{0x3c003c00u + (uint32_t)lane, 0x3c00u, 0x3800u + (uint32_t)s, 0x3c00u};
+        }
+        q1[s] = q0[s] ^ 3u;
+    }
+    f32x16 acc[4] = {};
+    const float c = 0.228f, m = NOISE ? 2.0f : 0.5f;
+    for (int it = 0; it < iters; ++it) {
+        const int sub = it & 1;
+        f32x16 s0 = {}, s1 = {};
+#pragma unroll
+        for (int s = 0; s < 3; ++s) {
+            const u32x4 a = *(const u32x4*)(base + k_off + (32 * sub * D + 16 * s) * 2);
+            s0 = mm32(a, q0[s], s0);
+            s1 = mm32(a, q1[s], s1);
+        }
+        u32x4 p0[2], p1[2];
+        tile_softmax<EXPS>(s0, c, m, p0);
+        tile_softmax<EXPS>(s1, c, m, p1);
+        if constexpr (NOISE) {   // keep P realistic: no growth of O from iteration to iteration
+            acc[0] *= 0.5f;
+            acc[2] *= 0.5f;
+        }
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+            for (int n = 0; n < 2; ++n) {
+                const char* vb = base + v_off + (32 * sub + 16 * u) * D * 2 + n * 64;
+                const u32x2 lo = lds_read_tr(vb);
+                const u32x2 hi = lds_read_tr(vb + 8 * D * 2);
+                const u32x4 a = {lo[0], lo[1], hi[0], hi[1]};
+                acc[n] = mm32(a, p0[u], acc[n]);
+                acc[2 + n] = mm32(a, p1[u], acc[2 + n]);
+            }
+    }
+    float s = 0.0f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s += acc[0][r] + acc[1][r] + acc[2][r] + acc[3][r];
+    return s;
+}
+
+__global__ __launch_bounds__(512, 2) void tile_kernel(float* __restrict__ out, int iters, int mode) {
+    float s;
+    switch (mode) {
+        case 0: s = tile_mix<false, false>(iters); break;
+        case 1: s = tile_mix<true, false>(iters); break;
+        case 2: s = tile_mix<false, true>(iters); break;
+        default: s = tile_mix<true, true>(iters); break;
+    }
+    out[(size_t)blockIdx.x * 512 + threadIdx.x] = s;
+}
+
 __global__ __launch_bounds__(512) void mix_kernel(float* __restrict__ out, int mode, int it_m, int it_v,
                                                   unsigned long long* __restrict__ clk) {
     const int wave = threadIdx.x >> 6;
@@ -155,6 +271,13 @@ extern "C" int sdattn_probe_mix(int mode, int blocks, int it_m, int it_v, float*
         it_m > (1 << 20) || it_v > (1 << 20))
         return (int)hipErrorInvalidValue;
     hipLaunchKernelGGL(mix_kernel, dim3(blocks), dim3(512), 0, (hipStream_t)stream, out, mode, it_m, it_v, clk);
+    return (int)hipGetLastError();
+}
+
+extern "C" int sdattn_probe_tile(int blocks, int iters, int mode, float* out, void* stream) {
+    if (!out || blocks < 1 || blocks > 65536 || iters < 1 || iters > (1 << 20) || mode < 0 || mode > 3)
+        return (int)hipErrorInvalidValue;
+    hipLaunchKernelGGL(tile_kernel, dim3(blocks), dim3(512), 0, (hipStream_t)stream, out, iters, mode);
     return (int)hipGetLastError();
 }
 

@@ -181,6 +181,10 @@ def main():
         mp = peaks["mfma_f16_tflops"]
         roofline["peak_measured"] = mp
         roofline["frac_measured"] = round(self_tflops / mp, 4)
+        # the matrix core alone on random operands: the ceiling with data that toggles
+        mpn = peaks["mfma_f16_noise_tflops"]
+        roofline["peak_measured_random_operands"] = mpn
+        roofline["frac_measured_random_operands"] = round(self_tflops / mpn, 4)
         hp = peaks["hbm_copy_gbs"]
         out["cross"]["peak_measured_gbs"] = hp
         out["cross"]["warm_frac_measured"] = round(cross_gbs / hp, 4)
@@ -343,6 +347,15 @@ def bench_block(torch, sd, wl, dev, stream, attn_ms, launches=50, reps=3):
                      "attention_us": round(attn_ms[kind] * 1e3, 2),
                      "projections_us": round((ms - attn_ms[kind]) * 1e3, 2),
                      "shape": f"x [{case.B},{case.Lq},{case.C}] ctx [{case.B},{case.Lk},{case.Cc}] H{case.H}"}
+        if kind == "self":
+            # the same projections through torch (hipBLASLt), for comparison only:
+            # Q, K, V as one [C, 3C] product and the output projection with bias
+            x2 = x.reshape(-1, case.C)
+            w3 = torch.cat([wq, wk, wv], 0).contiguous()
+            qkv_ms = timed(lambda: torch.nn.functional.linear(x2, w3))
+            out_ms = timed(lambda: torch.nn.functional.linear(x2, wo, bo))
+            res[kind]["torch_projections_us"] = {"qkv": round(qkv_ms * 1e3, 2), "out": round(out_ms * 1e3, 2),
+                                                 "total": round((qkv_ms + out_ms) * 1e3, 2)}
         if kind == "cross":
             D = case.C // case.H
             k = torch.empty(case.B, case.H, case.Lk, D, dtype=x.dtype, device=dev)
@@ -458,10 +471,17 @@ def measured_peaks(torch, dev, stream):
     mfma_f16_tflops    back-to-back v_mfma_f32_32x32x16_f16, two waves per SIMD
     shader_clock_ghz   the shader-clock counter against the 100 MHz counter
                        during that stream (clock under matrix-core load)
+    *_noise_*          the same on random operands (bits toggling like real
+                       activations) and the clock it sustains
     exp / fma          wave64 instructions per SIMD per shader cycle, alone
     overlap_*          time of one MFMA wave + one VALU wave per SIMD against
                        each alone: 0 = the sum of both (no overlap), 1 = the
                        longer of the two (full overlap)
+    tile_mix_*         the D = 40 self-attention tile's instructions without
+                       data movement, per 32x32 pair and SIMD, with and without
+                       exponentials, near-constant or toggling operands, the
+                       two waves of a SIMD in step or half an iteration apart;
+                       the shader clock during each and the cycles per pair
     hbm_*_gbs          1 GiB copy (read + write bytes / time) and 2 GiB read
     """
     from paper_2304_11267_amd import probes
@@ -478,13 +498,23 @@ def measured_peaks(torch, dev, stream):
     t0, t1, r0, r1 = (int(x) for x in clk.cpu().tolist())
     clock_ghz = (t1 - t0) / ((r1 - r0) / 100e6) / 1e9 if r1 > r0 else None
     mfma_tf = blocks * 8 * it_m * probes.MFMA_FLOPS_PER_ITER / (t_mfma * 1e-3) / 1e12
+    # the same stream on random operands (a realistic matrix-core ceiling: the
+    # clock it sustains drops with the bits that toggle)
+    clk.zero_()
+    t_mfma_n = run(probes.MIX_MFMA_NOISE, it_m, 0, clk)
+    t0, t1, r0, r1 = (int(x) for x in clk.cpu().tolist())
+    clock_n = (t1 - t0) / ((r1 - r0) / 100e6) / 1e9 if r1 > r0 else None
+    mfma_tf_n = blocks * 8 * it_m * probes.MFMA_FLOPS_PER_ITER / (t_mfma_n * 1e-3) / 1e12
     t_fma = run(probes.MIX_FMA, 0, it_v)
     t_exp = run(probes.MIX_EXP, 0, it_v // 2)
     simds = 256 * 4
     waves_per_simd = blocks * 8 / simds
     res = {"mfma_f16_tflops": round(mfma_tf, 1),
            "mfma_f16_frac_of_datasheet": round(mfma_tf / PEAK_F16_TFLOPS, 4),
-           "shader_clock_ghz": round(clock_ghz, 3) if clock_ghz else None}
+           "shader_clock_ghz": round(clock_ghz, 3) if clock_ghz else None,
+           "mfma_f16_noise_tflops": round(mfma_tf_n, 1),
+           "mfma_f16_noise_frac_of_datasheet": round(mfma_tf_n / PEAK_F16_TFLOPS, 4),
+           "shader_clock_noise_ghz": round(clock_n, 3) if clock_n else None}
     if clock_ghz:
         cyc = lambda ms: ms * 1e-3 * clock_ghz * 1e9
         res["fma_cycles_per_wave64_op"] = round(cyc(t_fma) / (waves_per_simd * it_v * 16), 2)
@@ -500,14 +530,34 @@ def measured_peaks(torch, dev, stream):
         res[f"overlap_mfma_{name}"] = round((hi - both) / (hi - lo), 3) if hi > lo else None
         res[f"mfma_{name}_us"] = {"mfma_alone": round(half_m * 1e3, 1), f"{name}_alone": round(alone_v * 1e3, 1),
                                   "together": round(both * 1e3, 1)}
-    # the D = 40 tile's instruction mix without data movement: ns per 32x32 pair per SIMD
+    # the D = 40 tile's instruction mix without data movement: ns per 32x32 pair per SIMD,
+    # the shader clock during it, and the shader cycles per pair at that clock
     ti = 4000
     pairs_per_simd = 2 * ti * 2           # two waves per SIMD, two pairs per iteration
+    tile_clock, tile_cycles = {}, {}
     for key, exps, noise in (("tile_mix_ns_per_pair", True, False), ("tile_mix_no_exp_ns_per_pair", False, False),
                              ("tile_mix_noise_ns_per_pair", True, True),
                              ("tile_mix_noise_no_exp_ns_per_pair", False, True)):
-        t = _events_ms(torch, stream, lambda: probes.tile(256, ti, exps, out, noise, stream))
+        clk.zero_()
+        t = _events_ms(torch, stream, lambda: probes.tile(256, ti, exps, out, noise, clk, stream))
         res[key] = round(t * 1e6 / pairs_per_simd, 2)
+        t0, t1, r0, r1 = (int(x) for x in clk.cpu().tolist())
+        if r1 > r0:
+            ghz = (t1 - t0) / ((r1 - r0) / 100e6) / 1e9
+            name = key[len("tile_mix_"):-len("_ns_per_pair")] or "plain"
+            tile_clock[name] = round(ghz, 3)
+            tile_cycles[name] = round(res[key] * ghz, 1)
+    # the same with the second wave of each SIMD started half an iteration late
+    clk.zero_()
+    t = _events_ms(torch, stream, lambda: probes.tile(256, ti, True, out, True, clk, stream, stagger=13))
+    res["tile_mix_noise_staggered_ns_per_pair"] = round(t * 1e6 / pairs_per_simd, 2)
+    t0, t1, r0, r1 = (int(x) for x in clk.cpu().tolist())
+    if r1 > r0:
+        ghz = (t1 - t0) / ((r1 - r0) / 100e6) / 1e9
+        tile_clock["noise_staggered"] = round(ghz, 3)
+        tile_cycles["noise_staggered"] = round(res["tile_mix_noise_staggered_ns_per_pair"] * ghz, 1)
+    res["tile_mix_clock_ghz"] = tile_clock
+    res["tile_mix_cycles_per_pair"] = tile_cycles
     # HBM streaming (buffers far beyond the 256 MB Infinity Cache)
     n = 1 << 30
     src = torch.empty(n, dtype=torch.uint8, device=dev)
@@ -528,9 +578,10 @@ def measured_peaks(torch, dev, stream):
 
 def cross_floor(torch, wl, dev, stream, case, nsets=40):
     """The cross-attention kernel's bytes moved by a plain copy with its grid
-    (256-row workgroups of eight waves, each reading its head's K and V and
-    copying its Q rows to O), inputs rotated over `nsets` sets as in the cold
-    protocol: the floor for any kernel that moves those bytes that way."""
+    (workgroups of 8, 4 or 2 waves of 32 query rows, each reading its head's K
+    and V and copying its Q rows to O), inputs rotated over `nsets` sets as in
+    the cold protocol: the floor for any kernel that moves those bytes that
+    way; and Q to O as one plain copy, the floor for moving them at all."""
     from paper_2304_11267_amd import probes
     sets = []
     g = torch.Generator(device=dev)
@@ -565,9 +616,33 @@ def cross_floor(torch, wl, dev, stream, case, nsets=40):
                                 "cold_gbs": round(case.bytes / (cold * 1e-3) / 1e9, 1),
                                 "warm_us": round(warm * 1e3, 3),
                                 "warm_gbs": round(case.bytes / (warm * 1e-3) / 1e9, 1)}
+    # Q -> O as one plain grid-stride copy (no K, V; 2048 workgroups of 256
+    # threads, 16 bytes per lane): what the chip does with these bytes at best
+    qbytes = case.B * case.H * case.Lq * case.D * 2
+    blocks = 2048
+
+    def plain(rot):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(20_000_000)
+        e0.record(stream)
+        for i in range(launches):
+            s = sets[i % nsets] if rot else sets[0]
+            probes.copy(s[0], s[3], qbytes, blocks, stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / launches
+
+    for s in sets:
+        probes.copy(s[0], s[3], qbytes, blocks, stream)
+    torch.cuda.synchronize()
+    cold = min(plain(True) for _ in range(3))
+    warm = min(plain(False) for _ in range(3))
+    res["plain_copy"] = {"cold_us": round(cold * 1e3, 3), "cold_gbs": round(2 * qbytes / (cold * 1e-3) / 1e9, 1),
+                         "warm_us": round(warm * 1e3, 3), "warm_gbs": round(2 * qbytes / (warm * 1e-3) / 1e9, 1),
+                         "bytes": 2 * qbytes}
     res["what"] = ("plain copy of Q to O plus reads of K, V in workgroups of 8, 4 or 2 strips of 32 rows "
-                   f"(the cross kernel launches 8), {nsets} rotated input sets (cold) or one (warm), "
-                   "back-to-back launches")
+                   f"(the cross kernel launches 4), {nsets} rotated input sets (cold) or one (warm), "
+                   "back-to-back launches; plain_copy: Q to O alone, grid-stride over 2048 workgroups")
     return res
 
 

@@ -28,11 +28,14 @@ extern "C" {
  *   mode 2: every wave EXP             mode 3: waves 0-3 MFMA, 4-7 FMA
  *   mode 4: waves 0-3 MFMA, 4-7 EXP    mode 5: waves 0-3 MFMA, 4-7 idle
  *   mode 6: waves 0-3 idle, 4-7 FMA    mode 7: waves 0-3 idle, 4-7 EXP
+ *   mode 8: every wave MFMA on random operands (four distinct A and B
+ *           operands in turn, bits that toggle like real activations; the
+ *           other modes use near-constant ones)
  * out: blocks * 512 floats (a checksum per lane, keeps the streams live).
  * clk: 4 values from the first wave of workgroup 0: the shader-clock counter
  *      (s_memtime) and the constant 100 MHz counter (s_memrealtime) at the
  *      start and at the end of its stream; may be NULL.
- * Limits: 1 <= blocks <= 65536, 0 <= it_m, it_v <= 1 << 20. */
+ * Limits: 0 <= mode <= 8, 1 <= blocks <= 65536, 0 <= it_m, it_v <= 1 << 20. */
 int sdattn_probe_mix(int mode, int blocks, int it_m, int it_v, float* out,
                      unsigned long long* clk, void* stream);
 
@@ -43,10 +46,16 @@ int sdattn_probe_mix(int mode, int blocks, int it_m, int it_v, float* out,
  * per pair 16 v_fma_f32, 16 v_exp_f32 and 8 conversions, V^T by
  * transposing LDS reads into 2 x 4 MFMAs.  mode bit 0: with the
  * exponentials; bit 1: operands of random sign and mantissa (bits that toggle
- * like real activations) instead of near-constant ones.
- * out: blocks * 512 floats.  Limits: 1 <= blocks <= 65536, 1 <= iters <= 1 << 20,
- * 0 <= mode <= 3. */
-int sdattn_probe_tile(int blocks, int iters, int mode, float* out, void* stream);
+ * like real activations) instead of near-constant ones.  The second wave of
+ * each SIMD (waves 4-7) starts `stagger` x 64 cycles after the first, to
+ * shift the two waves' phases against each other.
+ * out: blocks * 512 floats.
+ * clk: 4 values from the first wave of workgroup 0, as for sdattn_probe_mix
+ *      (the shader clock under this mix); may be NULL.
+ * Limits: 1 <= blocks <= 65536, 1 <= iters <= 1 << 20, 0 <= mode <= 3,
+ * 0 <= stagger <= 64. */
+int sdattn_probe_tile(int blocks, int iters, int mode, int stagger, float* out, unsigned long long* clk,
+                      void* stream);
 
 /* dst[0 .. bytes) = src[0 .. bytes) with 16-byte loads and stores, grid-stride
  * over `blocks` workgroups of 256 threads.  bytes % 16 == 0, pointers 16-byte

@@ -14,20 +14,45 @@
 namespace sdattn {
 namespace {
 
-// Four independent 32x32x16 f16 accumulators: back-to-back matrix-core work.
+// fp16 pairs of random sign and mantissa with magnitudes in [1/4, 2): operand
+// bits that toggle like real activations (the matrix core's power, and so the
+// clock it sustains, depends on them)
+__device__ __forceinline__ uint32_t noise_h2(uint32_t i) {
+    const uint32_t h = i * 2654435761u ^ (i >> 7) * 40503u;
+    const uint32_t lo = (h & 0x83ffu) | (0x3400u + ((h >> 10) & 0x0c00u));
+    const uint32_t g = h * 2246822519u;
+    const uint32_t hi = (g & 0x83ffu) | (0x3400u + ((g >> 10) & 0x0c00u));
+    return lo | (hi << 16);
+}
+
+// Four independent 32x32x16 f16 accumulators: back-to-back matrix-core work,
+// on near-constant operands or (NOISE) on four random A and B operands taken
+// in turn, so that the inputs of consecutive MFMAs differ.
+template <bool NOISE>
 __device__ __forceinline__ float mfma_stream(int iters) {
-    f16x8 a, b;
+    f16x8 a[4], b[4];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        a[i] = (_Float16)((threadIdx.x & 63) * 0.001f);
-        b[i] = (_Float16)0.5f;
-    }
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            if constexpr (NOISE) {
+                const uint32_t k = 64u * (uint32_t)(threadIdx.x * 4 + j) + 2u * (uint32_t)i;
+                const uint32_t x = noise_h2(k), y = noise_h2(k + 1);
+                a[j][2 * i] = __builtin_bit_cast(_Float16, (uint16_t)x);
+                a[j][2 * i + 1] = __builtin_bit_cast(_Float16, (uint16_t)(x >> 16));
+                b[j][2 * i] = __builtin_bit_cast(_Float16, (uint16_t)y);
+                b[j][2 * i + 1] = __builtin_bit_cast(_Float16, (uint16_t)(y >> 16));
+            } else {
+                a[j][2 * i] = a[j][2 * i + 1] = (_Float16)((threadIdx.x & 63) * 0.001f);
+                b[j][2 * i] = b[j][2 * i + 1] = (_Float16)0.5f;
+            }
+        }
     f32x16 c0 = {}, c1 = {}, c2 = {}, c3 = {};
     for (int it = 0; it < iters; ++it) {
-        c0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c0, 0, 0, 0);
-        c1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c1, 0, 0, 0);
-        c2 = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c2, 0, 0, 0);
-        c3 = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c3, 0, 0, 0);
+        c0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[0], b[0], c0, 0, 0, 0);
+        c1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[NOISE ? 1 : 0], b[NOISE ? 1 : 0], c1, 0, 0, 0);
+        c2 = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[NOISE ? 2 : 0], b[NOISE ? 2 : 0], c2, 0, 0, 0);
+        c3 = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[NOISE ? 3 : 0], b[NOISE ? 3 : 0], c3, 0, 0, 0);
     }
     float s = 0.0f;
 #pragma unroll
@@ -88,19 +113,9 @@ __device__ __forceinline__ void tile_softmax(const f32x16& st, float c, float m,
         for (int w = 0; w < 4; ++w) p[u][w] = pack_h2(e[8 * u + 2 * w], e[8 * u + 2 * w + 1]);
 }
 
-// fp16 pairs of random sign and mantissa with magnitudes in [1/4, 2): operand
-// bits that toggle like real activations (the matrix core's power, and so the
-// clock it sustains, depends on them)
-__device__ __forceinline__ uint32_t noise_h2(uint32_t i) {
-    const uint32_t h = i * 2654435761u ^ (i >> 7) * 40503u;
-    const uint32_t lo = (h & 0x83ffu) | (0x3400u + ((h >> 10) & 0x0c00u));
-    const uint32_t g = h * 2246822519u;
-    const uint32_t hi = (g & 0x83ffu) | (0x3400u + ((g >> 10) & 0x0c00u));
-    return lo | (hi << 16);
-}
 
 template <bool EXPS, bool NOISE>
-__device__ float tile_mix(int iters) {
+__device__ float tile_mix(int iters, int stagger) {
     constexpr int D = 40;
     __shared__ __attribute__((aligned(16))) char lds[32 * 1024];
     for (int i = threadIdx.x; i < 32 * 1024 / 16; i += 512)
@@ -125,6 +140,9 @@ __device__ float tile_mix(int iters) {
     }
     f32x16 acc[4] = {};
     const float c = 0.228f, m = NOISE ? 2.0f : 0.5f;
+    // the second wave of each SIMD starts `stagger` x 64 cycles late
+    if (wave >= 4)
+        for (int z = 0; z < stagger; ++z) __builtin_amdgcn_s_sleep(1);
     for (int it = 0; it < iters; ++it) {
         const int sub = it & 1;
         f32x16 s0 = {}, s1 = {};
@@ -159,15 +177,30 @@ __device__ float tile_mix(int iters) {
     return s;
 }
 
-__global__ __launch_bounds__(512, 2) void tile_kernel(float* __restrict__ out, int iters, int mode) {
+__global__ __launch_bounds__(512, 2) void tile_kernel(float* __restrict__ out, int iters, int mode, int stagger,
+                                                       unsigned long long* __restrict__ clk) {
+    const bool first = blockIdx.x == 0 && threadIdx.x == 0;
+    unsigned long long t0 = 0, r0 = 0;
+    if (first) {
+        t0 = __builtin_amdgcn_s_memtime();
+        r0 = __builtin_amdgcn_s_memrealtime();
+    }
     float s;
     switch (mode) {
-        case 0: s = tile_mix<false, false>(iters); break;
-        case 1: s = tile_mix<true, false>(iters); break;
-        case 2: s = tile_mix<false, true>(iters); break;
-        default: s = tile_mix<true, true>(iters); break;
+        case 0: s = tile_mix<false, false>(iters, stagger); break;
+        case 1: s = tile_mix<true, false>(iters, stagger); break;
+        case 2: s = tile_mix<false, true>(iters, stagger); break;
+        default: s = tile_mix<true, true>(iters, stagger); break;
     }
     out[(size_t)blockIdx.x * 512 + threadIdx.x] = s;
+    if (first && clk) {
+        const unsigned long long t1 = __builtin_amdgcn_s_memtime();
+        const unsigned long long r1 = __builtin_amdgcn_s_memrealtime();
+        clk[0] = t0;
+        clk[1] = t1;
+        clk[2] = r0;
+        clk[3] = r1;
+    }
 }
 
 __global__ __launch_bounds__(512) void mix_kernel(float* __restrict__ out, int mode, int it_m, int it_v,
@@ -182,12 +215,13 @@ __global__ __launch_bounds__(512) void mix_kernel(float* __restrict__ out, int m
     const bool low = wave < 4;   // waves 0-3: one per SIMD; 4-7: the second of each SIMD
     float s = 0.0f;
     switch (mode) {
-        case 0: s = mfma_stream(it_m); break;
+        case 0: s = mfma_stream<false>(it_m); break;
+        case 8: s = mfma_stream<true>(it_m); break;
         case 1: s = valu_stream<0>(it_v); break;
         case 2: s = valu_stream<1>(it_v); break;
-        case 3: s = low ? mfma_stream(it_m) : valu_stream<0>(it_v); break;
-        case 4: s = low ? mfma_stream(it_m) : valu_stream<1>(it_v); break;
-        case 5: s = low ? mfma_stream(it_m) : 0.0f; break;
+        case 3: s = low ? mfma_stream<false>(it_m) : valu_stream<0>(it_v); break;
+        case 4: s = low ? mfma_stream<false>(it_m) : valu_stream<1>(it_v); break;
+        case 5: s = low ? mfma_stream<false>(it_m) : 0.0f; break;
         case 6: s = low ? 0.0f : valu_stream<0>(it_v); break;
         default: s = low ? 0.0f : valu_stream<1>(it_v); break;
     }
@@ -267,17 +301,19 @@ using namespace sdattn;
 
 extern "C" int sdattn_probe_mix(int mode, int blocks, int it_m, int it_v, float* out,
                                 unsigned long long* clk, void* stream) {
-    if (!out || mode < 0 || mode > 7 || blocks < 1 || blocks > 65536 || it_m < 0 || it_v < 0 ||
+    if (!out || mode < 0 || mode > 8 || blocks < 1 || blocks > 65536 || it_m < 0 || it_v < 0 ||
         it_m > (1 << 20) || it_v > (1 << 20))
         return (int)hipErrorInvalidValue;
     hipLaunchKernelGGL(mix_kernel, dim3(blocks), dim3(512), 0, (hipStream_t)stream, out, mode, it_m, it_v, clk);
     return (int)hipGetLastError();
 }
 
-extern "C" int sdattn_probe_tile(int blocks, int iters, int mode, float* out, void* stream) {
-    if (!out || blocks < 1 || blocks > 65536 || iters < 1 || iters > (1 << 20) || mode < 0 || mode > 3)
+extern "C" int sdattn_probe_tile(int blocks, int iters, int mode, int stagger, float* out,
+                                 unsigned long long* clk, void* stream) {
+    if (!out || blocks < 1 || blocks > 65536 || iters < 1 || iters > (1 << 20) || mode < 0 || mode > 3 ||
+        stagger < 0 || stagger > 64)
         return (int)hipErrorInvalidValue;
-    hipLaunchKernelGGL(tile_kernel, dim3(blocks), dim3(512), 0, (hipStream_t)stream, out, iters, mode);
+    hipLaunchKernelGGL(tile_kernel, dim3(blocks), dim3(512), 0, (hipStream_t)stream, out, iters, mode, stagger, clk);
     return (int)hipGetLastError();
 }
 

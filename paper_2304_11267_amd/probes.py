@@ -17,6 +17,7 @@ EXPORTS = ("sdattn_probe_mix", "sdattn_probe_tile", "sdattn_probe_copy", "sdattn
 MIX_MFMA, MIX_FMA, MIX_EXP = 0, 1, 2
 MIX_MFMA_FMA, MIX_MFMA_EXP = 3, 4
 MIX_MFMA_HALF, MIX_FMA_HALF, MIX_EXP_HALF = 5, 6, 7
+MIX_MFMA_NOISE = 8
 MFMA_FLOPS_PER_ITER = 4 * 2 * 32 * 32 * 16     # four 32x32x16 MFMAs per wave and iteration
 VALU_OPS_PER_ITER = 16
 
@@ -37,7 +38,7 @@ def load_library():
     lib = ctypes.CDLL(path)
     vp, i32, i64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_longlong
     lib.sdattn_probe_mix.argtypes = [i32, i32, i32, i32, vp, vp, vp]
-    lib.sdattn_probe_tile.argtypes = [i32, i32, i32, vp, vp]
+    lib.sdattn_probe_tile.argtypes = [i32, i32, i32, i32, vp, vp, vp]
     lib.sdattn_probe_copy.argtypes = [vp, vp, i64, i32, vp]
     lib.sdattn_probe_read.argtypes = [vp, i64, vp, i32, vp]
     lib.sdattn_probe_strip_copy.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp]
@@ -64,9 +65,10 @@ def mix(mode, blocks, it_m, it_v, out, clk=None, stream=None):
         ctypes.c_void_p(clk.data_ptr()) if clk is not None else None, _stream(stream)))
 
 
-def tile(blocks, iters, exps, out, noise=False, stream=None):
+def tile(blocks, iters, exps, out, noise=False, clk=None, stream=None, stagger=0):
     _check("sdattn_probe_tile", load_library().sdattn_probe_tile(
-        blocks, iters, (1 if exps else 0) | (2 if noise else 0), ctypes.c_void_p(out.data_ptr()), _stream(stream)))
+        blocks, iters, (1 if exps else 0) | (2 if noise else 0), stagger, ctypes.c_void_p(out.data_ptr()),
+        ctypes.c_void_p(clk.data_ptr()) if clk is not None else None, _stream(stream)))
 
 
 def copy(src, dst, nbytes, blocks, stream=None):

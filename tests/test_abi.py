@@ -375,8 +375,10 @@ def test_probe_library_exports_every_declared_symbol():
         assert hasattr(plib, name), name
     # out-of-range arguments are refused before any launch (hipErrorInvalidValue = 1)
     assert plib.sdattn_probe_mix(9, 1, 1, 1, QA, None, None) == 1
-    assert plib.sdattn_probe_tile(1, 0, 1, QA, None) == 1
-    assert plib.sdattn_probe_tile(1, 1, 4, QA, None) == 1
+    assert plib.sdattn_probe_mix(-1, 1, 1, 1, QA, None, None) == 1
+    assert plib.sdattn_probe_tile(1, 0, 1, 0, QA, None, None) == 1
+    assert plib.sdattn_probe_tile(1, 1, 4, 0, QA, None, None) == 1
+    assert plib.sdattn_probe_tile(1, 1, 1, 65, QA, None, None) == 1
     assert plib.sdattn_probe_copy(QA, KA, 15, 1, None) == 1
     assert plib.sdattn_probe_copy(QA, ctypes.c_void_p(0x10000010), 4096, 1, None) == 1   # overlap
     assert plib.sdattn_probe_read(QA, 0, KA, 1, None) == 1

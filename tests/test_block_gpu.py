@@ -58,6 +58,13 @@ LIN_SHAPES = [
     (1, 129, 40, 1280, 8),
     (1, 33, 1280, 1280, 8),
     (3, 10, 24, 16, 2),
+    # one 64-channel slice with sequences shorter than a 32-row store pass,
+    # three slices with head widths 48 / 40, the 64x64 level's 8192 token rows,
+    # and Q, K and V's 960 outputs in one product
+    (3, 10, 64, 80, 2),
+    (2, 300, 192, 160, 4),
+    (2, 4096, 320, 320, 8),
+    (1, 1000, 320, 960, 8),
 ]
 
 

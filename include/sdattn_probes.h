@@ -1,9 +1,11 @@
 /*
  * sdattn_probes.h -- C ABI of libsdattn_probes.so, the measurement kernels
  * behind the denominators the benchmark reports beside the datasheet peaks
- * (sustained fp16 matrix-core rate and shader clock, the exponential and FMA
- * rates and how each shares a SIMD with the matrix core, HBM streaming rates,
- * and a plain copy with the cross-attention kernel's grid and byte pattern).
+ * (sustained fp16 matrix-core rate and shader clock on near-constant and on
+ * random operands, the exponential and FMA rates and how each shares a SIMD
+ * with the matrix core, the self-attention tile's instruction mix, HBM
+ * streaming rates, and a plain copy with the cross-attention kernel's grid
+ * and byte pattern).
  *
  * None of these kernels computes anything of the attention; they exist so
  * that a roofline fraction can be read against what the chip sustains as

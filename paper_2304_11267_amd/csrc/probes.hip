@@ -2,10 +2,12 @@
 //
 // They compute nothing of the attention.  The benchmark runs them to report
 // what the chip sustains beside its published peaks: the fp16 matrix-core
-// rate and the shader clock under that load, the v_exp_f32 and v_fma_f32
-// rates and whether each runs while the matrix core of the same SIMD is busy,
-// HBM streaming rates, and a plain copy with the cross-attention kernel's
-// grid and byte pattern (the floor for a kernel that moves those bytes).
+// rate and the shader clock under that load (near-constant and random
+// operands), the v_exp_f32 and v_fma_f32 rates and whether each runs while
+// the matrix core of the same SIMD is busy, the self-attention tile's
+// instruction mix without its data movement, HBM streaming rates, and a plain
+// copy with the cross-attention kernel's grid and byte pattern (the floor for
+// a kernel that moves those bytes).
 // Every loop is bounded by its arguments and every access is inside the
 // caller's buffers.
 #include "device.h"

@@ -1,8 +1,8 @@
 """The attention block through the library's static scratch (no workspace,
 no allocation) against the same block with a caller workspace: identical
 kernels on identical inputs, so identical bits, on two calls in a row with
-the second smaller than the first.  Also held to the parity bound against the
-oracle chain on sampled rows."""
+the second smaller than the first (the workspace block itself is held to the
+oracle chain in test_block_gpu.py)."""
 import numpy as np
 import pytest
 

@@ -13,9 +13,12 @@
 //                    query per lane (lane % 32) and 16 of the 32 keys of a
 //                    sub-tile in that lane's registers, so the row max needs
 //                    one exchange between the lane halves (v_permlane32_swap).
-//   p = 2^(c s - m)  c = |scale| log2(e); m is a running row maximum that is
+//   p = 2^(c s - m)  c = |scale| log2(e); m is a running reference that is
 //                    only moved (with the matching rescale of O and l) when a
-//                    tile's maximum exceeds it by more than 8, so p <= 256.
+//                    tile's maximum exceeds it by more than 15, and then to
+//                    that maximum less 8: p <= 2^15 always, the largest
+//                    weights near 2^8, and weights down to 2^-32 of them
+//                    above fp16's smallest subnormal.
 //   O^T += V^T P^T   32x32x16 MFMA, A = V^T from a transposed LDS tile, B = P
 //                    straight from the S^T accumulator registers (no shuffle);
 //                    O^T again has one query per lane.
@@ -40,7 +43,8 @@ constexpr int kThreads = kWaves * 64;
 constexpr int kBQ = kWaves * 32;   // query rows per workgroup
 constexpr int kKB = 64;            // keys per LDS tile
 constexpr int kVS = kKB + 4;       // V^T row pitch in elements (conflict-free 8-byte reads)
-constexpr float kRescaleSlack = 8.0f;
+constexpr float kPBias = 8.0f;          // m = a logit maximum less this
+constexpr float kRescaleLimit = 15.0f;  // largest weight before m moves: 2^15
 
 // K tile row pitch (elements): D rounded so that pitch/8 is odd, which keeps
 // the 16-byte reads of 16 consecutive rows on distinct LDS banks.
@@ -219,8 +223,8 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_kernel(
         mloc = half_max(mloc);
         s_max = fmaxf(s_max, mloc);
         const float mb = mloc * c;
-        if (__any(mb > m_run + kRescaleSlack)) {
-            const float m_new = fmaxf(m_run, mb);
+        if (__any(mb > m_run + kRescaleLimit)) {
+            const float m_new = fmaxf(m_run, mb - kPBias);
             const float alpha = fast_exp2(m_run - m_new);
 #pragma unroll
             for (int n = 0; n < DN; ++n)

@@ -22,12 +22,15 @@
 //                    16 of the 32 keys in that lane, so the row maximum needs a
 //                    single exchange between lane halves.
 //   p = 2^(c s - m)  c = |scale| log2(e), one FMA and one exponential per
-//                    score.  m is fixed at the maximum of each
-//                    wave's first sub-tile (p may then exceed 1); a row whose
-//                    later logits would overflow the rounded p sends the
+//                    score.  m is fixed at the maximum of each wave's first
+//                    sub-tile less kPBias = 8 (p may then exceed 1); a row
+//                    whose later logits would overflow the rounded p sends the
 //                    workgroup through an exact fallback in which m moves, with
-//                    the rescale of O and l, when a sub-tile's maximum exceeds
-//                    it by more than 8.
+//                    the rescale of O and l, whenever a weight would pass 2^15.
+//                    The bias keeps the largest weights near 2^8 instead of 1,
+//                    so weights down to 2^-32 of the largest survive rounding
+//                    to fp16 (its subnormals end at 2^-24): on very long key
+//                    sequences their sum is otherwise lost.
 //   O^T += V^T P^T   32x32x16 MFMA.  B = P straight from the S^T registers;
 //                    A = V^T, produced from the row-major V tile by the
 //                    transposing LDS read ds_read_b64_tr_b16: 16 lanes each
@@ -68,7 +71,12 @@ namespace {
 constexpr int kGeoSmall = 0;           // 64 rows, 64-key tiles
 constexpr int kGeoNormal = 1;          // 128 rows, 64-key tiles
 constexpr int kGeoBig = 2;             // 256 rows, 128-key tiles (QB = 2 only)
-constexpr float kRescaleSlack = 8.0f;
+// The exponent's reference m sits kPBias below the logit maximum it was
+// taken from (weights of the largest logits near 2^8; see p = 2^(c s - m)
+// above); the online path moves m once a sub-tile's maximum would give a
+// weight above 2^kRescaleLimit (fp16 holds values below 2^16).
+constexpr float kPBias = 8.0f;
+constexpr float kRescaleLimit = 15.0f;
 constexpr int kMaxLds = 160 * 1024;
 
 // QB = 32-row query blocks per wave.  With QB = 2 every K and V^T operand
@@ -255,12 +263,15 @@ __global__ __launch_bounds__((Geom<D, GEO>::kThreads), (Geom<D, GEO>::kWavesPerS
     reset();
 
     // How a sub-tile treats the running maximum m (log2 units):
-    //   kFirst  the wave's first sub-tile: m = its row maximum (O is still 0)
+    //   kFirst  the wave's first sub-tile: m = its row maximum - kPBias (O is
+    //           still 0)
     //   kFixed  m stays; p = 2^(c s - m) may exceed 1, and if a later logit
-    //           exceeds m by more than ~16 the rounded p overflows to inf,
-    //           which the overflow vote after the loop detects
-    //   kOnline m moves (with the rescale of O and l) whenever a sub-tile's
-    //           maximum exceeds it by more than 8 -- the fallback
+    //           exceeds the first sub-tile's maximum by more than ~8 the
+    //           rounded p overflows to inf, which the overflow vote after the
+    //           loop detects
+    //   kOnline m moves (with the rescale of O and l) to a sub-tile's maximum
+    //           - kPBias whenever that maximum exceeds m by more than
+    //           kRescaleLimit -- the fallback
     enum { kFirst = 0, kFixed = 1, kOnline = 2 };
 
     // One 32-key sub-tile (keys kbase ..) held at row offset `sub` * 32 of
@@ -299,11 +310,11 @@ __global__ __launch_bounds__((Geom<D, GEO>::kThreads), (Geom<D, GEO>::kWavesPerS
                 mloc = half_max(mloc);
                 s_max[j] = fmaxf(s_max[j], mloc);
                 if constexpr (MODE == kFirst) {
-                    m_run[j] = mloc * c;
+                    m_run[j] = mloc * c - kPBias;
                 } else if constexpr (MODE == kOnline) {
                     const float mb = mloc * c;
-                    if (__any(mb > m_run[j] + kRescaleSlack)) {
-                        const float m_new = fmaxf(m_run[j], mb);
+                    if (__any(mb > m_run[j] + kRescaleLimit)) {
+                        const float m_new = fmaxf(m_run[j], mb - kPBias);
                         const float alpha = fast_exp2(m_run[j] - m_new);
 #pragma unroll
                         for (int n = 0; n < DN; ++n)
@@ -531,8 +542,9 @@ __global__ __launch_bounds__((Geom<D, GEO>::kThreads), (Geom<D, GEO>::kWavesPerS
     };
 
     run_tiles(fixed_c);
-    // Overflow vote: with m fixed at the first sub-tile's maximum, a later
-    // logit larger by more than ~16 (log2) overflows the rounded p to inf,
+    // Overflow vote: with m fixed at the first sub-tile's maximum - kPBias, a
+    // later logit larger than that maximum by more than ~8 (log2) overflows
+    // the rounded p to inf,
     // which makes this lane's row sum non-finite.  Any such row sends the
     // whole workgroup (it shares the LDS tiles) through the online path.
     {

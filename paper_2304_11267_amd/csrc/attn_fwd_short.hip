@@ -188,7 +188,10 @@ __global__ __launch_bounds__(W * 64) void attn_fwd_short_kernel(
 #pragma unroll
         for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, st[t][r]);
     const float s_max = half_max(mloc);
-    const float negm = -(s_max * c);
+    // weights 2^(c s - c s_max + 8): the largest 256 rather than 1, so that
+    // weights down to 2^-32 of it stay above fp16's smallest subnormal (the
+    // factor cancels in O / l and is taken out of S below)
+    const float negm = 8.0f - s_max * c;
 
     f32x16 acc[DN];
 #pragma unroll
@@ -282,7 +285,7 @@ __global__ __launch_bounds__(W * 64) void attn_fwd_short_kernel(
     if (LS && half == 0 && qvalid) {
         float* o2 = LS + ((size_t)bh * Lq + q0 + l32) * 2;
         o2[0] = s_max * scale_abs;
-        o2[1] = l;
+        o2[1] = l * (1.0f / 256.0f);
     }
 }
 

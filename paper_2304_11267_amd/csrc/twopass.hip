@@ -198,8 +198,11 @@ __global__ __launch_bounds__(256) void softmax_pv_kernel(const char* __restrict_
 
     const char* Vh = (const char*)(V + (size_t)bh * Lk * D);
     const char* arow = A + row * Lk * AS;
-    const float cL = LS[2 * row] * kLog2e;
-    const float Sinv = 1.0f / LS[2 * row + 1];
+    // weights exp(a - L) 2^8 (the largest 256 rather than 1, so that weights
+    // down to 2^-32 of it stay above fp16's smallest subnormal); the factor
+    // comes out with 1 / S
+    const float cL = LS[2 * row] * kLog2e - 8.0f;
+    const float Sinv = (1.0f / 256.0f) / LS[2 * row + 1];
     const int ntiles = (Lk + kPvK - 1) / kPvK;
 
     // V tile t into registers (rows past Lk are zero), then into LDS buffer b

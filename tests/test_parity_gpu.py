@@ -13,7 +13,7 @@ import oracle
 import paper_2304_11267_amd as sd
 from paper_2304_11267_amd import workloads as wl
 
-from parity_util import assert_close, to_device, to_host64
+from parity_util import accumulation_allowance, assert_close, to_device, to_host64
 
 pytestmark = pytest.mark.gpu
 
@@ -199,6 +199,110 @@ def test_one_hot_dominant_logit():
     lone = [i for i in range(Lq) if sum(1 for j in range(Lk) if j % D == i % D) == 1]
     for i in lone:
         assert np.max(np.abs(g[0, 0, i] - v[0, 0, i % D].astype(np.float64))) <= 2e-3
+
+
+def _long_keys_case(Lq, Lk, seed, planted):
+    """q, k, v ~ N(0, 1) fp16 drawn on the GPU (torch's generator, seeded), with
+    key j of each (row r, key j) in `planted` set to 4 q_r (exact in fp16):
+    its logit, 4 |q_r|^2 / sqrt(D), stands far above the rest, so row r's
+    output is led by v_j and a key read from the wrong place shows at once."""
+    import torch
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    D = 40
+    q = torch.randn(1, 1, Lq, D, dtype=torch.float16, device="cuda", generator=g)
+    k = torch.randn(1, 1, Lk, D, dtype=torch.float16, device="cuda", generator=g)
+    v = torch.randn(1, 1, Lk, D, dtype=torch.float16, device="cuda", generator=g)
+    for r, j in planted:
+        k[0, 0, j] = q[0, 0, r] * 4
+    return q, k, v
+
+
+def _check_long(q, k, v, rows, what):
+    # fp32 accumulation over Lk keys: the allowance of the tolerance grows as
+    # Lk 2^-28 past 4096 keys (parity_util)
+    import torch
+    scale = 1.0 / q.shape[3] ** 0.5
+    out = torch.empty_like(q)
+    sd.forward(q, k, v, out, scale)
+    out2 = torch.empty_like(q)
+    ls = torch.empty(q.shape[:3] + (2,), dtype=torch.float32, device="cuda")
+    sd.forward_ex(q, k, v, out2, scale, ls=ls)
+    torch.cuda.synchronize()
+    qh, kh, vh = (t.cpu().numpy() for t in (q, k, v))
+    r, L, S, dev = oracle.attention(qh, kh, vh, scale, rows=rows, want_dev=True)
+    D = q.shape[3]
+    Lk = k.shape[2]
+    for o, tag in ((out, " (plain)"), (out2, " (with statistics)")):
+        assert_close(to_host64(o).reshape(-1, D)[rows], r, what=what + tag, dev=dev, n_keys=Lk)
+    lsr = ls.cpu().numpy().astype(np.float64).reshape(-1, 2)[rows]
+    assert np.max(np.abs(lsr[:, 0] - L) / np.maximum(1.0, np.abs(L))) <= 1e-5
+    assert np.max(np.abs(lsr[:, 1] - S) / S) <= 2e-3 + accumulation_allowance(Lk)
+
+
+def test_a_million_keys_in_the_tiled_kernel():
+    # 1 000 003 keys (a ragged last tile) through the tiled kernel's 64-row
+    # workgroups; the planted keys sit in the last tile, mid-sequence and in
+    # the first sub-tile, so rows 0 and 1 also take the exact fallback
+    Lk = 1_000_003
+    q, k, v = _long_keys_case(256, Lk, 9301, [(0, Lk - 1), (1, Lk // 2), (2, 5)])
+    _check_long(q, k, v, np.array([0, 1, 2, 100, 255]), "1M keys")
+
+
+def test_key_byte_offsets_past_32_bits():
+    # 26 843 648 keys of D = 40: a head's K (and V) spans 2 147 491 840 bytes,
+    # past what 32-bit offsets address, so the call takes the general kernel
+    # (64-bit addressing).  Every key is zero (logit 0, value 0) except three
+    # planted ones, one past the 2 GiB mark: then Eq. 3 reduces to a sum over
+    # the planted keys plus (Lk - 3) e^-M in the denominator, evaluated here
+    # in fp64.  Each planted key k_j = a_r q_r (rounded to fp16; the reference
+    # takes the rounded values) has logit ln(Lk) + 14: it carries all but
+    # e^-14 of its row's weight, so its row's output is its value row, read
+    # from where it lies.
+    import torch
+    Lk, D, Lq = 26_843_648, 40, 64
+    assert Lk * D * 2 > 2 ** 31
+    scale = float(np.float32(1.0 / D ** 0.5))
+    rng = np.random.default_rng(9302)
+    q = rng.standard_normal((1, 1, Lq, D)).astype(np.float16)
+    planted = [(0, Lk - 1), (1, 20_000_000), (2, 3)]
+    kp, vp = [], []
+    for r, j in planted:
+        q64 = q[0, 0, r].astype(np.float64)
+        a = (np.log(Lk) + 14.0) / (scale * (q64 @ q64))
+        kp.append((q64 * a).astype(np.float16))
+        vp.append(rng.standard_normal(D).astype(np.float16))
+    qd = to_device(q)
+    k = torch.zeros(1, 1, Lk, D, dtype=torch.float16, device="cuda")
+    v = torch.zeros_like(k)
+    for (r, j), kj, vj in zip(planted, kp, vp):
+        k[0, 0, j] = torch.from_numpy(kj).cuda()
+        v[0, 0, j] = torch.from_numpy(vj).cuda()
+    out = torch.empty_like(qd)
+    sd.forward(qd, k, v, out, scale)
+    ls = torch.empty(1, 1, Lq, 2, dtype=torch.float32, device="cuda")
+    out2 = torch.empty_like(qd)
+    sd.forward_ex(qd, k, v, out2, scale, ls=ls)
+    torch.cuda.synchronize()
+    # Eq. 3 for this input: planted logits s_j, Lk - 3 logits of 0 with value 0
+    Kp = np.array(kp, np.float64)
+    Vp = np.array(vp, np.float64)
+    s = scale * (q[0, 0].astype(np.float64) @ Kp.T)                  # [Lq, 3]
+    M = np.maximum(0.0, s.max(axis=1))
+    e = np.exp(s - M[:, None])
+    Ssum = e.sum(axis=1) + (Lk - len(planted)) * np.exp(-M)
+    ref = (e @ Vp) / Ssum[:, None]
+    dev = (e[:, :, None] * np.abs(Vp[None] - ref[:, None])).sum(axis=1) / Ssum[:, None] \
+        + ((Lk - len(planted)) * np.exp(-M) / Ssum)[:, None] * np.abs(ref)
+    for o, tag in ((out, " (plain)"), (out2, " (with statistics)")):
+        assert_close(to_host64(o)[0, 0], ref, what="2 GiB of keys" + tag, dev=dev, n_keys=Lk)
+    lsr = ls.cpu().numpy().astype(np.float64)[0, 0]
+    assert np.max(np.abs(lsr[:, 0] - M) / np.maximum(1.0, M)) <= 1e-5
+    assert np.max(np.abs(lsr[:, 1] - Ssum) / Ssum) <= 2e-3 + accumulation_allowance(Lk)
+    # the planted rows are their value rows, to the fp16 rounding of the output
+    for r, _ in planted:
+        assert e[r].max() / Ssum[r] > 1 - 1e-6
+        assert np.max(np.abs(to_host64(out)[0, 0, r] - Vp[r]) / np.maximum(1.0, np.abs(Vp[r]))) <= 2e-3
 
 
 def test_joint_permutation_invariance_on_gpu():

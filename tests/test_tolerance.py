@@ -63,3 +63,12 @@ def test_one_percent_relative_error_fails_everywhere():
     g = r * 1.011
     with pytest.raises(AssertionError):
         assert_close(g, r, "f16", "planted")
+
+
+def test_accumulation_allowance_grows_past_4096_keys():
+    from parity_util import accumulation_allowance
+    # 16 keys per MFMA step, half an fp32 ulp (2^-24) per step
+    assert accumulation_allowance() == accumulation_allowance(4096) == 2.0 ** -16
+    assert accumulation_allowance(77) == 2.0 ** -16
+    assert accumulation_allowance(1 << 20) == (1 << 20) / 16 * 2.0 ** -24
+    assert accumulation_allowance(26_843_648) > 0.09

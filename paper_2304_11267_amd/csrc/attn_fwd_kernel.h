@@ -4,7 +4,8 @@
 // One workgroup covers 128 query rows of one (batch, head) (64 or 256 in the
 // other geometries, see Geom).  Its waves are
 // split in two halves over the key tiles (the first half of the tiles and the
-// second), and at the end the two halves of every row are merged through LDS.
+// second; four quarters in one geometry), and at the end the parts of every
+// row are merged through LDS.
 // A wave owns QB blocks of 32 query rows: QB = 2 when D <= 64 (4 waves per
 // workgroup), QB = 1 above (8 waves).  With QB = 2 every K and V^T operand
 // read from LDS feeds two MFMAs.  Registers are budgeted for two waves per
@@ -71,6 +72,7 @@ namespace {
 constexpr int kGeoSmall = 0;           // 64 rows, 64-key tiles
 constexpr int kGeoNormal = 1;          // 128 rows, 64-key tiles
 constexpr int kGeoBig = 2;             // 256 rows, 128-key tiles (QB = 2 only)
+constexpr int kGeoQuarter = 3;         // 64 rows, keys split four ways, 64-key tiles
 // The exponent's reference m sits kPBias below the logit maximum it was
 // taken from (weights of the largest logits near 2^8; see p = 2^(c s - m)
 // above); the online path moves m once a sub-tile's maximum would give a
@@ -78,6 +80,7 @@ constexpr int kGeoBig = 2;             // 256 rows, 128-key tiles (QB = 2 only)
 constexpr float kPBias = 8.0f;
 constexpr float kRescaleLimit = 15.0f;
 constexpr int kMaxLds = 160 * 1024;
+constexpr int kQuarterMinKeys = 512;   // shortest key sequence given to kGeoQuarter
 
 // QB = 32-row query blocks per wave.  With QB = 2 every K and V^T operand
 // read from LDS feeds two MFMAs (half the LDS traffic per flop) and each wave
@@ -90,25 +93,32 @@ constexpr int kMaxLds = 160 * 1024;
 // eight waves) and the keys per tile (128), for grids that still cover the
 // CUs: each K/V tile then serves twice the queries and a barrier twice the
 // keys, in the LDS the two 128-row workgroups of a CU would otherwise hold.
+// kGeoQuarter keeps kGeoSmall's 64 rows but splits the keys four ways
+// instead of two (eight waves), for small grids whose LDS would otherwise
+// leave one wave per SIMD: two waves then share each SIMD and hide each
+// other's MFMA and exponential latencies.  Its tiles carry no constant
+// block (the LDS holds four splits' double buffers), so l comes from v_dot2.
 template <int D, int GEO = kGeoNormal>
 struct Geom {
     static constexpr int QB = D <= 64 ? 2 : 1;
     static constexpr bool kBig = GEO == kGeoBig;
+    static constexpr bool kQuarter = GEO == kGeoQuarter;
+    static constexpr int kKS = kQuarter ? 4 : 2;              // key splits
     static constexpr int kTK = kBig ? 128 : 64;               // keys per LDS tile
-    static constexpr int kQW = kBig ? 4 : (GEO == kGeoSmall ? 2 : 4) / QB;   // query waves
+    static constexpr int kQW = kBig ? 4 : (GEO == kGeoSmall || kQuarter ? 2 : 4) / QB;   // query waves
     static constexpr int kBQ = 32 * QB * kQW;                 // query rows per workgroup
-    static constexpr int kWaves = 2 * kQW;                    // times two key halves
+    static constexpr int kWaves = kKS * kQW;                  // times the key splits
     static constexpr int kThreads = kWaves * 64;
     static constexpr int DK = (D + 15) / 16;                  // 16-deep k steps of Q K^T
     static constexpr int DN = (D + 31) / 32;                  // 32-row d tiles of O^T
-    static constexpr bool kOnes = (D % 32) != 0;              // padding rows carry the row sum
+    static constexpr bool kOnes = (D % 32) != 0 && !kQuarter;   // padding rows carry the row sum
     static constexpr int kTileBytes = kTK * D * 2;            // one K or V tile
     static constexpr int kChunks = kTileBytes / 1024;         // 1 KiB wave copies per tile
     static constexpr int kBufBytes = kTileBytes * (kOnes ? 3 : 2);   // K, V (, constant block)
-    static constexpr int kHalfBytes = 2 * kBufBytes;          // two buffers per key half
+    static constexpr int kHalfBytes = 2 * kBufBytes;          // two buffers per key split
     static constexpr int kMergeFloats = QB * (DN * 16 * 64 + 3 * 64);   // one wave's O^T, m, max, l
-    static constexpr int kMergeBytes = kQW * kMergeFloats * 4;
-    static constexpr int kLdsBytes = 2 * kHalfBytes > kMergeBytes ? 2 * kHalfBytes : kMergeBytes;
+    static constexpr int kMergeBytes = (kKS - 1) * kQW * kMergeFloats * 4;
+    static constexpr int kLdsBytes = kKS * kHalfBytes > kMergeBytes ? kKS * kHalfBytes : kMergeBytes;
     static constexpr bool kFits = D >= 32 && D % 8 == 0 && kLdsBytes <= kMaxLds && (!kBig || QB == 2);
     // Waves per SIMD the register budget is sized for: two (256 registers
     // each) when the LDS lets enough workgroups share a CU, else one, which
@@ -139,7 +149,7 @@ __global__ __launch_bounds__((Geom<D, GEO>::kThreads), (Geom<D, GEO>::kWavesPerS
     const int l32 = lane & 31;
     const int half = lane >> 5;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int kh = wave / kQW;         // key half of this wave
+    const int kh = wave / kQW;         // key split ("half" when there are two) of this wave
     const int wq = wave % kQW;         // query slot of this wave
 
     const int tile = xcd_remap(blockIdx.x, gridDim.x);
@@ -149,13 +159,13 @@ __global__ __launch_bounds__((Geom<D, GEO>::kThreads), (Geom<D, GEO>::kWavesPerS
 
     const char* Kh = (const char*)(K + (size_t)bh * Lk * D);
     const char* Vh = (const char*)(V + (size_t)bh * Lk * D);
-    char* hbase = smem + kh * G::kHalfBytes;   // this half's two buffers
+    char* hbase = smem + kh * G::kHalfBytes;   // this split's two buffers
 
     // Constant blocks (one per buffer): a one in column 0 of every row, zeros
     // elsewhere.  Lanes whose d lies at or past D read these instead of V.
     if constexpr (G::kOnes) {
         const uint32_t one = from_float<ET>(1.0f);
-        for (int i = tid; i < 4 * (TB / 16); i += kThreads) {
+        for (int i = tid; i < 2 * G::kKS * (TB / 16); i += kThreads) {
             const int b = i / (TB / 16), j = i - b * (TB / 16);
             u32x4 w = {0u, 0u, 0u, 0u};
             if ((j * 8) % D == 0) w[0] = one;
@@ -163,13 +173,14 @@ __global__ __launch_bounds__((Geom<D, GEO>::kThreads), (Geom<D, GEO>::kWavesPerS
         }
     }
 
-    // Tiles of this half: [t_first, t_first + t_count).  Half 0 takes the
-    // first ceil(ntiles / 2), half 1 the rest; both run nh steps.
+    // Tiles of this split: [t_first, t_first + t_count).  Split s takes
+    // tiles s * nh .. s * nh + nh - 1 (nh = ceil(ntiles / kKS)), the last
+    // ones what remains, possibly none; all run nh steps.
     constexpr int kTK = G::kTK;
     const int ntiles = (Lk + kTK - 1) / kTK;
-    const int nh = (ntiles + 1) / 2;
-    const int t_first = kh ? nh : 0;
-    const int t_count = kh ? ntiles - nh : nh;
+    const int nh = (ntiles + G::kKS - 1) / G::kKS;
+    const int t_first = kh * nh;
+    const int t_count = min(nh, max(0, ntiles - t_first));
 
     // Copy tile t of this half into its buffer b (the half's kQW waves issue
     // the 1 KiB pieces wq, wq + kQW, ...).  Rows past Lk repeat row Lk - 1
@@ -240,7 +251,10 @@ __global__ __launch_bounds__((Geom<D, GEO>::kThreads), (Geom<D, GEO>::kWavesPerS
 #pragma unroll
         for (int n = 0; n < DN; ++n) {
             const int ds = 32 * n + 16 * (g & 1) + 4 * (i & 3);
-            v_off[n] = ds < D ? TB + (krow * D + ds) * 2 : 2 * TB + (krow * D + ds - D) * 2;
+            // past D: the constant block, or (without one) V columns 32
+            // lower, whose finite products land in O^T rows never stored
+            v_off[n] = ds < D ? TB + (krow * D + ds) * 2
+                              : G::kOnes ? 2 * TB + (krow * D + ds - D) * 2 : TB + (krow * D + ds - 32) * 2;
         }
     }
 
@@ -581,10 +595,12 @@ __global__ __launch_bounds__((Geom<D, GEO>::kThreads), (Geom<D, GEO>::kWavesPerS
         }
     }
 
-    // ---- merge the two key halves of every row (the block-merge rule)
+    // ---- merge the key splits of every row (the block-merge rule): split s
+    // > 0 leaves its O^T, m, max and l in LDS, split 0 folds them in
     constexpr int kMF = DN * 16 * 64 + 3 * 64;   // floats per query block
-    float* mrg = (float*)smem + wq * G::kMergeFloats;
-    if (kh == 1) {
+    auto mrg_of = [&](int s) { return (float*)smem + ((s - 1) * kQW + wq) * G::kMergeFloats; };
+    if (kh != 0) {
+        float* mrg = mrg_of(kh);
 #pragma unroll
         for (int j = 0; j < QB; ++j) {
             float* mj = mrg + j * kMF;
@@ -598,13 +614,15 @@ __global__ __launch_bounds__((Geom<D, GEO>::kThreads), (Geom<D, GEO>::kWavesPerS
         }
     }
     __syncthreads();
-    if (kh == 1) return;
+    if (kh != 0) return;
+#pragma unroll
+    for (int s = 1; s < G::kKS; ++s)
 #pragma unroll
     for (int j = 0; j < QB; ++j) {
-        const float* mj = mrg + j * kMF;
+        const float* mj = mrg_of(s) + j * kMF;
         const float m_b = mj[DN * 16 * 64 + lane];
         const float m_new = fmaxf(m_run[j], m_b);
-        const float a0 = fast_exp2(m_run[j] - m_new);   // exp2(-inf) = 0 for an empty half
+        const float a0 = fast_exp2(m_run[j] - m_new);   // exp2(-inf) = 0 for an empty split
         const float a1 = fast_exp2(m_b - m_new);
 #pragma unroll
         for (int n = 0; n < DN; ++n)
@@ -690,8 +708,17 @@ hipError_t launch_d(const AttnArgs& a) {
         const bool small = heads * ((a.Lq + 127) / 128) < 256;
         bool big = false;
         if constexpr (Geom<D, kGeoBig>::kFits) big = heads * ((a.Lq + 255) / 256) >= 256;
-        if (small) return a.o_rows ? launch_kernel<ET, D, false, true, kGeoSmall>(a)
-                                   : launch_kernel<ET, D, false, false, kGeoSmall>(a);
+        if (small) {
+            // keys split four ways (two waves per SIMD) once every split has
+            // at least two tiles
+            if constexpr (Geom<D, kGeoQuarter>::kFits) {
+                if (a.Lk >= kQuarterMinKeys)
+                    return a.o_rows ? launch_kernel<ET, D, false, true, kGeoQuarter>(a)
+                                    : launch_kernel<ET, D, false, false, kGeoQuarter>(a);
+            }
+            return a.o_rows ? launch_kernel<ET, D, false, true, kGeoSmall>(a)
+                            : launch_kernel<ET, D, false, false, kGeoSmall>(a);
+        }
         if constexpr (Geom<D, kGeoBig>::kFits) {
             if (big) return a.o_rows ? launch_kernel<ET, D, false, true, kGeoBig>(a)
                                      : launch_kernel<ET, D, false, false, kGeoBig>(a);

@@ -525,3 +525,63 @@ def test_bitwise_deterministic_at_the_64x64_level():
     q, k, v = wl.case_inputs(case)
     outs = [run_forward(q, k, v, case.scale) for _ in range(3)]
     assert np.array_equal(outs[0], outs[1]) and np.array_equal(outs[0], outs[2])
+
+
+# ------------- 64-row workgroups with the keys split four ways (eight waves):
+# the plain launch's geometry for grids of fewer than 256 128-row blocks once
+# Lk >= 512 and D <= 80 (the 32x32 level).  Split s takes tiles s*nh ..
+# s*nh + nh - 1 (nh = ceil(ntiles / 4)); the last splits may be short or
+# empty.  These tiles carry no constant block, so the row sum comes from
+# v_dot2 and the padded d rows read V columns that are never stored.
+
+QUARTER = [
+    # (B, H, Lq, Lk, D, dtype)
+    (1, 2, 200, 700, 80, "f16"),    # 11 tiles: 3 + 3 + 3 + 2, ragged last tile
+    (1, 2, 130, 513, 40, "f16"),    # 9 tiles: 3 + 3 + 3 + 0, last tile one key
+    (2, 1, 100, 1000, 56, "f16"),
+    (1, 3, 64, 600, 72, "f16"),
+    (1, 1, 97, 2048, 32, "f16"),
+    (1, 1, 33, 4100, 64, "f16"),    # 65 tiles: 17 + 17 + 17 + 14
+    (1, 2, 160, 777, 48, "bf16"),
+    (1, 2, 96, 1024, 80, "bf16"),
+]
+
+
+@pytest.mark.parametrize("shape", QUARTER, ids=lambda s: "x".join(map(str, s)))
+def test_quarter_key_split_geometry(shape):
+    B, H, Lq, Lk, D, dtype = shape
+    q, k, v = wl.make_qkv(B, H, Lq, Lk, D, 6100 + Lq + 3 * Lk + D, dtype=dtype)
+    check_case(q, k, v, float(np.float32(1 / np.sqrt(D))), dtype=dtype, what=f"quarter {shape}")
+
+
+@pytest.mark.parametrize("Lk,D,dtype", [(700, 80, "f16"), (1024, 40, "f16"), (513, 64, "f16"),
+                                        (1500, 80, "bf16")])
+def test_quarter_geometry_late_dominant_keys_fall_back(Lk, D, dtype):
+    """Keys past the first 32-key sub-tile of every one of the four splits
+    dominate in the even heads: the eight-wave vote sends the workgroup
+    through the online rerun and the four-way merge."""
+    B, H, Lq = 1, 4, 150
+    rng = np.random.default_rng(6200 + Lk + D)
+    q = np.zeros((B, H, Lq, D), np.float32)
+    q[..., 0] = 8.0
+    q[..., 1:] = rng.standard_normal((B, H, Lq, D - 1), dtype=np.float32) * 0.1
+    k = rng.standard_normal((B, H, Lk, D), dtype=np.float32) * 0.1
+    v = rng.standard_normal((B, H, Lk, D), dtype=np.float32)
+    nh = ((Lk + 63) // 64 + 3) // 4
+    for s in range(4):
+        j = s * nh * 64 + 40
+        if j < Lk:
+            k[:, ::2, j, 0] = 8.0
+    k[:, ::2, Lk - 1, 0] = 8.0
+    if dtype == "bf16":
+        q, k, v = (wl.to_bf16_bits(t) for t in (q, k, v))
+    else:
+        q, k, v = (t.astype(np.float16) for t in (q, k, v))
+    check_case(q, k, v, 1.0, dtype=dtype, what=f"quarter late-dominant Lk={Lk} D={D} {dtype}")
+
+
+def test_quarter_geometry_bitwise_deterministic():
+    case = wl.CASES["l32_self"]
+    q, k, v = wl.case_inputs(case)
+    outs = [run_forward(q, k, v, case.scale) for _ in range(3)]
+    assert np.array_equal(outs[0], outs[1]) and np.array_equal(outs[0], outs[2])

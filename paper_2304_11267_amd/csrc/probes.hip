@@ -157,10 +157,6 @@ __device__ float tile_mix(int iters, int stagger) {
         u32x4 p0[2], p1[2];
         tile_softmax<EXPS>(s0, c, m, p0);
         tile_softmax<EXPS>(s1, c, m, p1);
-        if constexpr (NOISE) {   // keep P realistic: no growth of O from iteration to iteration
-            acc[0] *= 0.5f;
-            acc[2] *= 0.5f;
-        }
 #pragma unroll
         for (int u = 0; u < 2; ++u)
 #pragma unroll

@@ -91,6 +91,16 @@ def test_unet_case_bf16(name):
     check_case(q, k, v, case.scale, dtype="bf16", what=name + "/bf16")
 
 
+@pytest.mark.parametrize("name,per_head", [("l32_self", 48), ("l64_self", 24)])
+def test_unet_case_bf16_sampled_rows(name, per_head):
+    """The 32x32 self-attention (64-row workgroups, keys split four ways) and
+    the 64x64 one (256-row workgroups, 128-key tiles) in bf16."""
+    case = wl.CASES[name]
+    q, k, v = wl.case_inputs(case, dtype="bf16")
+    rows = wl.sample_rows(case.B, case.H, case.Lq, per_head, seed=case.seed + 7)
+    check_case(q, k, v, case.scale, dtype="bf16", rows=rows, what=name + "/bf16")
+
+
 RAGGED = [
     # (B, H, Lq, Lk, D)
     (1, 1, 1, 1, 40),

@@ -7,7 +7,7 @@
 // second; four quarters in one geometry), and at the end the parts of every
 // row are merged through LDS.
 // A wave owns QB blocks of 32 query rows: QB = 2 when D <= 64 (4 waves per
-// workgroup), QB = 1 above (8 waves).  With QB = 2 every K and V^T operand
+// 128-row workgroup), QB = 1 above (8 waves).  With QB = 2 every K and V^T operand
 // read from LDS feeds two MFMAs.  Registers are budgeted for two waves per
 // SIMD (256 each), or for one (up to 512) where the LDS already limits a CU
 // to one wave per SIMD.
@@ -37,18 +37,19 @@
 //                    transposing LDS read ds_read_b64_tr_b16: 16 lanes each
 //                    point at 4 consecutive d of one key, and every lane gets
 //                    4 consecutive keys of one d.
-//   l                row sum of the rounded p.  When D is not a multiple of 32,
-//                    the lanes whose d lies past D read a constant block
-//                    instead of V: a one at d = D and zeros beyond, so the P V
-//                    product also yields l in row D of O^T.  Otherwise the
-//                    packed p pairs are summed with v_dot2 against (1, 1).
+//   l                row sum of the rounded p.  When D is not a multiple of 32
+//                    (and the LDS has room for it), the lanes whose d lies past
+//                    D read a constant block instead of V: a one at d = D and
+//                    zeros beyond, so the P V product also yields l in row D of
+//                    O^T.  Otherwise the packed p pairs are summed with v_dot2
+//                    against (1, 1).
 //
 // With the maximum fixed, a whole 64-key tile is written as a software
 // pipeline, so that each step's softmax has the independent MFMAs of its
 // neighbours beside it, and left to the compiler's scheduler.
 //
 // This is the block-wise ("multi-stage") reduction of Sec. 3.2.1 -- a block's
-// maximum and exponential sum merged into the running pair, and the two key
+// maximum and exponential sum merged into the running pair, and the key
 // halves merged by the same rule -- fused with the element-wise normalisation
 // and the product with V, so the N x M matrix A never leaves the chip (the
 // IO-aware tiling of FlashAttention, Sec. 3.2.2).
@@ -182,7 +183,7 @@ __global__ __launch_bounds__((Geom<D, GEO>::kThreads), (Geom<D, GEO>::kWavesPerS
     const int t_first = kh * nh;
     const int t_count = min(nh, max(0, ntiles - t_first));
 
-    // Copy tile t of this half into its buffer b (the half's kQW waves issue
+    // Copy tile t of this split into its buffer b (the split's kQW waves issue
     // the 1 KiB pieces wq, wq + kQW, ...).  Rows past Lk repeat row Lk - 1
     // (finite data; their weights are forced to zero).
     auto issue_tile = [&](int t, int b) __attribute__((always_inline)) {
@@ -510,9 +511,10 @@ __global__ __launch_bounds__((Geom<D, GEO>::kThreads), (Geom<D, GEO>::kWavesPerS
         // the loop body the accumulators keep their registers across
         // iterations instead of being copied at a join.
         // With 128-key tiles on the fixed-maximum path the workgroup also
-        // meets between the two 64-key halves of every tile (measured faster:
-        // 65.9 -> 64.9 us median at the 64x64 level); that barrier sits
-        // outside the conditions so every wave of both key halves reaches it.
+        // meets between the two 64-key halves of every tile (faster at the
+        // 64x64 level while the tile's steps were fenced, neutral since);
+        // that barrier sits outside the conditions so every wave of both key
+        // halves reaches it.
         constexpr bool kMidBarrier = G::kBig && decltype(mode_c)::value == kFixed && !STATS;
         int pend = -1;
         for (int i = 1; i < nh; ++i) {

@@ -177,6 +177,15 @@ def test_scale_values(scale):
     check_case(q, k, v, scale, what=f"scale={scale}")
 
 
+@pytest.mark.parametrize("scale", [0.0, -0.2, 1.0])
+@pytest.mark.parametrize("Lk,D", [(600, 80), (2100, 40)])
+def test_scale_values_long_keys(scale, Lk, D):
+    """Zero, negative and large scales through the tiled kernel's key loop
+    (64 query rows with the keys split four ways)."""
+    q, k, v = wl.make_qkv(1, 2, 100, Lk, D, 905 + Lk)
+    check_case(q, k, v, scale, what=f"scale={scale} Lk={Lk} D={D}")
+
+
 def test_constant_keys_give_mean_of_values():
     q, k, v = wl.make_qkv(1, 2, 130, 100, 40, 902)
     k[:] = k[:, :, :1]

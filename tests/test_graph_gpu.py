@@ -1,5 +1,6 @@
 """HIP graph capture of the library's launches.  Every forward path (the tiled
-kernel in its 256- and 64-row geometries, with and without the Eq. 4
+kernel in its 256- and 64-row geometries (the latter with two and with four
+key splits), with and without the Eq. 4
 statistics, the short-key kernel, the general kernel, bf16) and the
 no-allocation attention block record into a graph -- nothing in them
 allocates, clears memory or synchronises -- and every replay reproduces the
@@ -49,7 +50,8 @@ def _replays_match(record, outputs, reps=3):
 FORWARD_CASES = [
     (2, 8, 4096, 4096, 40, "f16", False),   # 256-row workgroups, 128-key tiles
     (1, 2, 300, 333, 40, "f16", True),      # 128-row workgroups with (L, S), ragged tiles
-    (2, 8, 1024, 1024, 80, "f16", False),   # 64-row workgroups
+    (2, 8, 1024, 1024, 80, "f16", False),   # 64-row workgroups, keys split four ways
+    (2, 8, 1024, 300, 80, "f16", False),    # 64-row workgroups, two key halves
     (2, 8, 4096, 77, 40, "f16", False),     # short-key kernel
     (1, 3, 70, 90, 16, "f16", False),       # general kernel
     (1, 2, 200, 260, 64, "bf16", True),
